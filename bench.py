@@ -1,0 +1,230 @@
+"""Benchmark one sparse-embedding training step on one MI355X.
+
+A step is the whole hot path on one synthetic batch: tc_embed_forward,
+tc_cast_index, tc_embed_backward and tc_sparse_update, back to back on one
+stream, with inputs already resident in HBM. Prints ONE JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config c2]
+
+Default workload: 8 tables x 1M rows x 64 fp32, batch 2048, 80 Zipf(1.05)
+indices per bag, SGD (configuration "c2"). Other configurations: c1..c5.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+NUM_BATCHES = 4        # distinct pre-generated batches the timed steps cycle through
+
+
+def algorithmic_bytes(w, n, u, nbags):
+    """Bytes each call must move at minimum under the paper's analytic model
+    (every gather counted once, Sec. III-C): index reads, row reads, row writes."""
+    D4 = 4 * w.dim
+    fwd = n * 4 + (nbags + 1) * 4 + n * D4 + nbags * D4
+    cast = n * 4 + (nbags + 1) * 4 + n * 4 + u * 4 + (u + 1) * 4
+    bwd = n * 4 + (u + 1) * 4 + n * D4 + u * D4
+    rows_rw = 3 if w.optimizer == "sgd" else 5   # G, W in, W out (+ A in, A out)
+    upd = u * 4 + rows_rw * u * D4
+    return {"forward": fwd, "cast": cast, "backward": bwd, "update": upd}
+
+
+KERNEL_SOURCES = {
+    "forward": "tc_gather_reduce.hip",
+    "backward": "tc_gather_reduce.hip",
+    "update": "tc_update.hip",
+    "cast": "tc_cast.hip",
+}
+KERNEL_NAMES = {
+    "forward": "k_gather_reduce (forward)",
+    "backward": "k_gather_reduce (backward)",
+    "update": "k_sparse_update",
+    "cast": "tc_cast_index (9+ kernels)",
+}
+
+
+def source_sha(call: str) -> str:
+    p = os.path.join(ROOT, "paper_2010_13100_amd", "csrc", KERNEL_SOURCES[call])
+    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+
+
+def load_traffic(call: str, workload: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel source (else None)."""
+    p = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(p):
+        return None
+    entry = json.load(open(p)).get(f"{call}:{workload}")
+    if not entry or entry.get("source_sha") != source_sha(call):
+        return None
+    return entry["hbm_bytes_per_launch"]
+
+
+def cpu_baseline(w, batch, budget_s: float):
+    """The fp32 oracle (single thread) on the same workload: forward, baseline
+    expand + coalesce backward, casting, update, on the rows batch 0 touches."""
+    import numpy as np
+
+    import oracle
+    from paper_2010_13100_amd import workload as wl
+    orc = oracle.Oracle("f32")
+    t = np.repeat(np.arange(w.num_bags) // w.batch, np.diff(batch.bag_offsets))
+    ids = np.unique(batch.table_row_offset[t] + batch.indices)
+    table = wl.table_rows(w, ids)
+    steps, t0 = 0, time.perf_counter()
+    phases: dict = {}
+    while True:
+        oracle.train_step(orc, num_tables=w.num_tables, bags_per_table=w.batch,
+                          table_row_offset=batch.table_row_offset, indices=batch.indices,
+                          bag_offsets=batch.bag_offsets, grad_out=batch.grad_out, table=table,
+                          table_ids=ids, optimizer=w.optimizer, lr=np.float32(w.lr),
+                          eps=np.float32(w.eps), timings=phases)
+        steps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or steps >= 50:
+            break
+    return {"value": steps / el, "unit": "steps/s", "cores": 1, "kind": "oracle",
+            "sample": f"{steps} full steps of batch 0 ({batch.num_pairs} pairs), fp32 oracle, "
+                      f"table rows restricted to the {len(ids)} rows the batch touches",
+            "seconds_per_phase": {k: round(v / steps, 4) for k, v in phases.items()}}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="seconds of oracle work for cpu_baseline (0 disables)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the hot path is built and timed on a single "
+              "MI355X; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2010_13100_amd import device_fill, tc
+    from paper_2010_13100_amd import workload as wl
+
+    w = wl.WORKLOADS[args.config]
+    print(f"[bench] workload {args.config} {w.name}: generating {NUM_BATCHES} batches",
+          file=sys.stderr, flush=True)
+    batches = [wl.make_batch(w, step=s) for s in range(NUM_BATCHES)]
+    max_pairs = max(b.num_pairs for b in batches)
+    dev = torch.device("cuda", 0)
+    trainer = tc.EmbeddingTrainer(total_rows=w.total_rows, dim=w.dim, num_tables=w.num_tables,
+                                  bags_per_table=w.batch, max_pairs=max_pairs,
+                                  optimizer=w.optimizer, lr=w.lr, eps=w.eps, device=dev)
+    device_fill.fill_uniform(trainer.W, seed=0, lo=w.init_lo, hi=w.init_hi)
+    dbat = [dict(off=torch.from_numpy(b.table_row_offset).to(dev),
+                 idx=torch.from_numpy(b.indices).to(dev),
+                 bo=torch.from_numpy(b.bag_offsets).to(dev),
+                 grad=torch.from_numpy(b.grad_out).to(dev), n=b.num_pairs) for b in batches]
+    stream = torch.cuda.current_stream(dev)
+
+    def step(i, ev=None):
+        d = dbat[i % NUM_BATCHES]
+        if ev is not None:
+            ev[0].record(stream)
+        trainer.forward(d["off"], d["idx"], d["bo"], stream)
+        if ev is not None:
+            ev[1].record(stream)
+        trainer.cast(d["off"], d["idx"], d["bo"], d["n"], stream)
+        if ev is not None:
+            ev[2].record(stream)
+        trainer.backward(d["grad"], stream)
+        if ev is not None:
+            ev[3].record(stream)
+        trainer.update(stream)
+        if ev is not None:
+            ev[4].record(stream)
+
+    print(f"[bench] warmup {args.warmup} steps", file=sys.stderr, flush=True)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for i in range(args.steps):
+        step(args.warmup + i, evs[i])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_total = start.elapsed_time(stop)
+    ms_step = ms_total / args.steps
+    calls = ["forward", "cast", "backward", "update"]
+    per_call_ms = {c: float(np.mean([e[k].elapsed_time(e[k + 1]) for e in evs]))
+                   for k, c in enumerate(calls)}
+    print(f"[bench] timed {args.steps} steps: {ms_step:.4f} ms/step (wall {wall:.3f} s)",
+          file=sys.stderr, flush=True)
+
+    # unique rows per batch (read once, outside the timed region)
+    uniq = []
+    for i in range(NUM_BATCHES):
+        d = dbat[i]
+        trainer.cast(d["off"], d["idx"], d["bo"], d["n"], stream)
+        uniq.append(int(trainer.num_unique.item()))
+    nbytes = {c: 0.0 for c in calls}
+    for i in range(args.steps):
+        b = (args.warmup + i) % NUM_BATCHES
+        for c, v in algorithmic_bytes(w, dbat[b]["n"], uniq[b], w.num_bags).items():
+            nbytes[c] += v / args.steps
+    step_bytes = sum(nbytes.values())
+
+    single = ["forward", "backward", "update"]
+    dom = max(single, key=lambda c: per_call_ms[c])
+    achieved = nbytes[dom] / (per_call_ms[dom] * 1e-3) / 1e9
+    traffic = load_traffic(dom, args.config)
+    result = {
+        "metric": "embedding train steps/sec (fwd+cast+bwd+update) and achieved HBM GB/s",
+        "value": round(args.steps / (ms_total * 1e-3), 3),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded Zipf/uniform index streams, N(0,1) output gradients, "
+                "SplitMix64 table init)",
+        "config": {"workload": f"{args.config}: {w.name}", "tables": w.num_tables,
+                   "rows_per_table": w.rows_per_table, "dim": w.dim, "batch": w.batch,
+                   "pairs_per_step": round(float(np.mean([d["n"] for d in dbat])), 1),
+                   "unique_rows_per_step": round(float(np.mean(uniq)), 1),
+                   "optimizer": w.optimizer},
+        "step_algorithmic_GBps": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
+        "step_algorithmic_frac_of_hbm_peak": round(step_bytes / (ms_step * 1e-3) / 1e9
+                                                   / HBM_PEAK_GBS, 4),
+        "per_call_us": {c: round(v * 1e3, 2) for c, v in per_call_ms.items()},
+        "per_call_algorithmic_GBps": {c: round(nbytes[c] / (per_call_ms[c] * 1e-3) / 1e9, 1)
+                                      for c in calls},
+        "roofline": {"bound": "hbm", "kernel": KERNEL_NAMES[dom],
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic},
+    }
+    if args.cpu_budget > 0:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(w, batches[0], args.cpu_budget)
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

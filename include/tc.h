@@ -1,0 +1,170 @@
+/*
+ * tc.h -- C-ABI of the Tensor Casting sparse-embedding training library for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * One training step of sparse embedding layers is four calls, in stream
+ * order (Kwon, Lee, Rhu, "Tensor Casting: Co-Designing Algorithm-Architecture
+ * for Personalized Recommendation Training", arXiv 2010.13100):
+ *
+ *   tc_embed_forward   embedding gather-reduce (Sec. II-B): pooled row sums
+ *   tc_cast_index      Tensor Casting (Algorithm 2, Sec. IV-A)
+ *   tc_embed_backward  casted gradient gather-reduce (Algorithm 3)
+ *   tc_sparse_update   gradient scatter with SGD or Adagrad (Sec. II-B, Eq. 2)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Pointers are DEVICE pointers owned by the caller unless a comment says
+ * "host". The library never allocates or frees device memory, never
+ * synchronises the stream and never copies to the host; scratch memory comes
+ * from the caller's workspace (tc_cast_workspace_bytes). Buffers must stay
+ * alive until the stream has finished the call.
+ *
+ * Every call is asynchronous on `stream` (a hipStream_t; NULL is the legacy
+ * default stream) and returns a tc_status. Host-side argument checks run
+ * before anything is launched; on such an error nothing is launched and no
+ * output is touched. A failed launch returns TC_ERR_HIP. tc_last_error()
+ * then gives a message for the calling thread.
+ *
+ * Layout
+ *  - Tables: T tables of the same width `dim` (fp32) are stored as one
+ *    row-major array of `total_rows` x `dim` floats. Table t owns global rows
+ *    [table_row_offset[t], table_row_offset[t+1]); `table_row_offset` is a
+ *    device int64 array of T+1 entries with table_row_offset[T] = total_rows.
+ *  - The index array of (src, dst) pairs (Sec. II-B) is bag-major CSR:
+ *    bag g = t * bags_per_table + b holds pairs bag_offsets[g] ..
+ *    bag_offsets[g+1]-1 (device int32, T*B+1 entries, non-decreasing,
+ *    bag_offsets[0] = 0, bag_offsets[T*B] = num_pairs); `indices[j]` is the
+ *    table-local row of pair j. src of pair j is table_row_offset[t] +
+ *    indices[j], dst is g.
+ *  - `dim` must be a multiple of 4 in [4, 1024], and every float pointer must
+ *    be 16-byte aligned (TC_ERR_UNSUPPORTED otherwise); num_pairs and
+ *    total_rows must be below 2^31.
+ *  - Out-of-range indices or malformed offsets are not detected and give
+ *    undefined results.
+ *
+ * Arithmetic: fp32 values, fp32 accumulation. Sums are taken one term after
+ * another, from +0, in the order of the index array (forward) or of the
+ * casted index (backward); results do not depend on the launch configuration
+ * and repeat bit for bit.
+ *
+ * Thread safety: no global state besides the per-thread error message;
+ * concurrent calls on different streams with different buffers are safe.
+ */
+#ifndef TC_H
+#define TC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TC_ABI_VERSION 1
+
+typedef enum tc_status {
+    TC_OK = 0,
+    TC_ERR_INVALID_ARG = 1,  /* null pointer with a non-zero size, negative size, ... */
+    TC_ERR_UNSUPPORTED = 2,  /* dim or alignment outside what the kernels handle */
+    TC_ERR_WORKSPACE = 3,    /* workspace missing or smaller than tc_cast_workspace_bytes */
+    TC_ERR_HIP = 4           /* a HIP launch failed; see tc_last_error() */
+} tc_status;
+
+typedef enum tc_opt_kind {
+    TC_OPT_SGD = 0,      /* W <- W - lr*G */
+    TC_OPT_ADAGRAD = 1   /* Eq. (2): A <- A + G*G; W <- W - lr*G/sqrt(eps + A) */
+} tc_opt_kind;
+
+/*
+ * Forward embedding gather-reduce (Sec. II-B, forward propagation).
+ * For every bag g: out[g, :] = sum over its pairs j, in order, of
+ * W[table_row_offset[g / bags_per_table] + indices[j], :], starting from +0.
+ * An empty bag gives a row of zeros.
+ *   W        [total_rows x dim] fp32 table (read only)
+ *   out      [num_tables*bags_per_table x dim] fp32 (written)
+ */
+tc_status tc_embed_forward(const float *W, int64_t total_rows, int32_t dim,
+                           const int64_t *table_row_offset, int32_t num_tables,
+                           int32_t bags_per_table, const int32_t *indices,
+                           const int32_t *bag_offsets, float *out, hipStream_t stream);
+
+/*
+ * Workspace bytes tc_cast_index needs for `num_pairs` pairs over
+ * `total_rows` global rows (host function; launches nothing).
+ */
+size_t tc_cast_workspace_bytes(int64_t num_pairs, int64_t total_rows);
+
+/*
+ * Tensor Casting (Algorithm 2). The (src, dst) pairs are sorted by src with
+ * a stable sort (equal src keep their input order, so with bag-major input
+ * the result is the (row, bag) lexicographic order). Then
+ *   casted_src[i] = dst of the i-th sorted pair (its bag id)
+ *   casted_dst[i] = (number of distinct src among sorted pairs 0..i) - 1
+ * and, per coalesced row u < U (U = number of distinct src):
+ *   unique_rows[u] = its global row (strictly increasing in u)
+ *   seg_offsets[u] = first sorted position of that row; seg_offsets[U] = num_pairs
+ *   *num_unique    = U (device int32; never copied to the host)
+ * Capacities: casted_src and casted_dst hold num_pairs entries; unique_rows
+ * holds min(num_pairs, total_rows) and seg_offsets one more. casted_dst may
+ * be NULL (the backward pass does not need it). All outputs are int32 and
+ * exact. `workspace` is device memory of at least
+ * tc_cast_workspace_bytes(num_pairs, total_rows) bytes, 256-byte aligned.
+ */
+tc_status tc_cast_index(const int64_t *table_row_offset, int32_t num_tables,
+                        int32_t bags_per_table, int64_t total_rows, const int32_t *indices,
+                        const int32_t *bag_offsets, int64_t num_pairs, int32_t *unique_rows,
+                        int32_t *seg_offsets, int32_t *casted_src, int32_t *casted_dst,
+                        int32_t *num_unique, void *workspace, size_t workspace_bytes,
+                        hipStream_t stream);
+
+/*
+ * Casted gradient gather-reduce (Algorithm 3): for every u < *num_unique,
+ *   coal_grad[u, :] = sum over i in [seg_offsets[u], seg_offsets[u+1]), in
+ *                     order, of grad_out[casted_src[i], :], starting from +0.
+ * This is the coalesced gradient of table row unique_rows[u]; the expanded
+ * per-pair gradient is never formed.
+ *   grad_out   [num_bags x dim] fp32, one gradient per pooled output
+ *   max_unique capacity of coal_grad in rows (>= *num_unique), normally
+ *              min(num_pairs, total_rows)
+ *   coal_grad  [max_unique x dim] fp32; rows >= *num_unique are not written
+ */
+tc_status tc_embed_backward(const float *grad_out, int32_t num_bags, int32_t dim,
+                            const int32_t *seg_offsets, const int32_t *casted_src,
+                            const int32_t *num_unique, int64_t max_unique, float *coal_grad,
+                            hipStream_t stream);
+
+/*
+ * Gradient scatter + optimizer (Sec. II-B; Adagrad is Eq. 2). For every
+ * u < *num_unique, with r = unique_rows[u] and G = coal_grad[u, :], elementwise:
+ *   TC_OPT_SGD:     t = lr*G;  W[r] = W[r] - t
+ *   TC_OPT_ADAGRAD: A[r] = A[r] + G*G;  s = sqrt(eps + A[r]);  q = G/s;
+ *                   W[r] = W[r] - lr*q
+ * each a separately rounded fp32 operation (no fused multiply-add; division
+ * and square root correctly rounded). Rows not in unique_rows are untouched,
+ * which equals a dense update with zero gradient for these optimizers.
+ *   W          [total_rows x dim] fp32 table (read-modify-write)
+ *   opt_state  Adagrad accumulator A, same shape as W (read-modify-write);
+ *              must be NULL for SGD
+ *   unique_rows must be distinct (as tc_cast_index produces them).
+ */
+tc_status tc_sparse_update(float *W, float *opt_state, int64_t total_rows, int32_t dim,
+                           const int32_t *unique_rows, const float *coal_grad,
+                           const int32_t *num_unique, int64_t max_unique, int32_t opt_kind,
+                           float lr, float eps, hipStream_t stream);
+
+/* Static text for a status code. */
+const char *tc_status_string(tc_status status);
+
+/* Message of the calling thread's last failed call ("" if none). */
+const char *tc_last_error(void);
+
+/* TC_ABI_VERSION of the loaded library. */
+int32_t tc_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TC_H */

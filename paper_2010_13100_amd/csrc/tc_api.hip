@@ -1,0 +1,42 @@
+// Status codes, per-thread error messages and launch checks of libtc.
+#include <cstdarg>
+
+#include "tc_internal.h"
+
+namespace tc {
+namespace {
+thread_local char g_error[512] = "";
+}
+
+void set_error(const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_error, sizeof(g_error), fmt, ap);
+    va_end(ap);
+}
+
+void clear_error() { g_error[0] = '\0'; }
+
+tc_status check_launch(const char *what) {
+    const hipError_t e = hipGetLastError();
+    if (e == hipSuccess) return TC_OK;
+    set_error("%s: %s", what, hipGetErrorString(e));
+    return TC_ERR_HIP;
+}
+
+}  // namespace tc
+
+extern "C" const char *tc_status_string(tc_status status) {
+    switch (status) {
+        case TC_OK: return "TC_OK";
+        case TC_ERR_INVALID_ARG: return "TC_ERR_INVALID_ARG";
+        case TC_ERR_UNSUPPORTED: return "TC_ERR_UNSUPPORTED";
+        case TC_ERR_WORKSPACE: return "TC_ERR_WORKSPACE";
+        case TC_ERR_HIP: return "TC_ERR_HIP";
+    }
+    return "TC_ERR_UNKNOWN";
+}
+
+extern "C" const char *tc_last_error(void) { return tc::g_error; }
+
+extern "C" int32_t tc_abi_version(void) { return TC_ABI_VERSION; }

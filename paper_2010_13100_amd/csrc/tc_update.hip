@@ -1,0 +1,123 @@
+// Gradient scatter with SGD or Adagrad (Sec. II-B; Adagrad is Eq. 2).
+//
+// Every coalesced row u has exactly one owner: a group of LANES lanes that
+// reads coal_grad[u], reads and writes W[unique_rows[u]] (and the Adagrad
+// accumulator row) with dwordx4 accesses. unique_rows are distinct, so no
+// atomics are needed and the result does not depend on scheduling. The
+// optimizer arithmetic is separately rounded fp32 (the library is built with
+// -ffp-contract=off; division and square root are correctly rounded).
+#include "tc_internal.h"
+
+namespace tc {
+namespace {
+
+template <int LANES, int CHUNKS, int OPT>
+__global__ __launch_bounds__(kBlock) void k_sparse_update(
+    float *__restrict__ W, float *__restrict__ A, int32_t dim,
+    const int32_t *__restrict__ rows, const float *__restrict__ coal,
+    const int32_t *__restrict__ num_unique_dev, int64_t cap, float lr, float eps) {
+    constexpr int kGroups = kWave / LANES;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int sub = lane & (LANES - 1);
+    const int grp = lane / LANES;
+    const int64_t nu = *num_unique_dev;
+    const int64_t num = nu < cap ? nu : cap;
+    const int64_t wave = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / kWave;
+    const int64_t nwave = (int64_t(gridDim.x) * blockDim.x) / kWave;
+    const int d4 = dim >> 2;
+
+    for (int64_t u0 = wave * kGroups; u0 < num; u0 += nwave * kGroups) {
+        const int64_t u = u0 + grp;
+        if (u >= num) continue;
+        const int64_t r = rows[u];
+        float *wrow = W + r * int64_t(dim);
+        const float *grow = coal + u * int64_t(dim);
+#pragma unroll
+        for (int c = 0; c < CHUNKS; ++c) {
+            const int col4 = sub + c * LANES;
+            if (col4 >= d4) continue;
+            const float4 g = *reinterpret_cast<const float4 *>(grow + 4 * col4);
+            float4 w = *reinterpret_cast<const float4 *>(wrow + 4 * col4);
+            if (OPT == TC_OPT_SGD) {
+                w.x = w.x - lr * g.x;
+                w.y = w.y - lr * g.y;
+                w.z = w.z - lr * g.z;
+                w.w = w.w - lr * g.w;
+            } else {
+                float *arow = A + r * int64_t(dim);
+                float4 a = *reinterpret_cast<const float4 *>(arow + 4 * col4);
+                a.x = a.x + g.x * g.x;
+                a.y = a.y + g.y * g.y;
+                a.z = a.z + g.z * g.z;
+                a.w = a.w + g.w * g.w;
+                w.x = w.x - lr * (g.x / sqrtf(eps + a.x));
+                w.y = w.y - lr * (g.y / sqrtf(eps + a.y));
+                w.z = w.z - lr * (g.z / sqrtf(eps + a.z));
+                w.w = w.w - lr * (g.w / sqrtf(eps + a.w));
+                *reinterpret_cast<float4 *>(arow + 4 * col4) = a;
+            }
+            *reinterpret_cast<float4 *>(wrow + 4 * col4) = w;
+        }
+    }
+}
+
+template <int OPT>
+tc_status launch_update(float *W, float *A, int32_t dim, const int32_t *rows, const float *coal,
+                        const int32_t *num_unique, int64_t cap, float lr, float eps,
+                        hipStream_t stream) {
+    const RowShape s = row_shape(dim);
+    const int64_t rows_per_block = (kBlock / kWave) * (kWave / s.lanes);
+    const unsigned grid = grid_for(cap, rows_per_block, int64_t(kNumCUs) * 8);
+#define TC_UP_CASE(L, C)                                                                 \
+    if (s.lanes == L && s.chunks == C) {                                                 \
+        k_sparse_update<L, C, OPT><<<grid, kBlock, 0, stream>>>(W, A, dim, rows, coal,    \
+                                                                num_unique, cap, lr, eps); \
+        return check_launch("k_sparse_update");                                          \
+    }
+    TC_UP_CASE(1, 1)
+    TC_UP_CASE(2, 1)
+    TC_UP_CASE(4, 1)
+    TC_UP_CASE(8, 1)
+    TC_UP_CASE(16, 1)
+    TC_UP_CASE(32, 1)
+    TC_UP_CASE(64, 1)
+    TC_UP_CASE(64, 2)
+    TC_UP_CASE(64, 3)
+    TC_UP_CASE(64, 4)
+#undef TC_UP_CASE
+    set_error("no update kernel for dim %d", dim);
+    return TC_ERR_UNSUPPORTED;
+}
+
+}  // namespace
+}  // namespace tc
+
+using namespace tc;
+
+extern "C" tc_status tc_sparse_update(float *W, float *opt_state, int64_t total_rows, int32_t dim,
+                                      const int32_t *unique_rows, const float *coal_grad,
+                                      const int32_t *num_unique, int64_t max_unique,
+                                      int32_t opt_kind, float lr, float eps,
+                                      hipStream_t stream) {
+    clear_error();
+    TC_REQUIRE(total_rows >= 0 && max_unique >= 0, TC_ERR_INVALID_ARG,
+               "tc_sparse_update: negative size");
+    TC_REQUIRE(total_rows < (int64_t(1) << 31) && max_unique < (int64_t(1) << 31),
+               TC_ERR_INVALID_ARG, "tc_sparse_update: sizes must be below 2^31");
+    TC_REQUIRE(dim > 0 && dim % 4 == 0 && dim <= kMaxDim, TC_ERR_UNSUPPORTED,
+               "tc_sparse_update: dim %d must be a multiple of 4 in [4, %d]", dim, kMaxDim);
+    TC_REQUIRE(opt_kind == TC_OPT_SGD || opt_kind == TC_OPT_ADAGRAD, TC_ERR_INVALID_ARG,
+               "tc_sparse_update: unknown optimizer %d", opt_kind);
+    TC_REQUIRE((opt_kind == TC_OPT_SGD) == (opt_state == nullptr), TC_ERR_INVALID_ARG,
+               "tc_sparse_update: opt_state must be NULL for SGD and given for Adagrad");
+    if (max_unique == 0) return TC_OK;
+    TC_REQUIRE(W && unique_rows && coal_grad && num_unique, TC_ERR_INVALID_ARG,
+               "tc_sparse_update: null pointer");
+    TC_REQUIRE(aligned16(W) && aligned16(coal_grad) && (!opt_state || aligned16(opt_state)),
+               TC_ERR_UNSUPPORTED, "tc_sparse_update: float pointers must be 16-byte aligned");
+    if (opt_kind == TC_OPT_SGD)
+        return launch_update<TC_OPT_SGD>(W, nullptr, dim, unique_rows, coal_grad, num_unique,
+                                         max_unique, lr, eps, stream);
+    return launch_update<TC_OPT_ADAGRAD>(W, opt_state, dim, unique_rows, coal_grad, num_unique,
+                                         max_unique, lr, eps, stream);
+}

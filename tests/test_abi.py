@@ -1,0 +1,169 @@
+"""The C-ABI library on the host: it loads, exports every declared entry
+point, and rejects bad arguments before launching anything (no GPU needed)."""
+import ctypes
+import glob
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2010_13100_amd import build as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER_LIBS = {"tc.h": "libtc.so", "tc_workload.h": "libtc_workload.so"}
+
+
+def declared_functions(header: str) -> list:
+    text = open(header).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tcw?_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def tc():
+    from paper_2010_13100_amd import tc as T
+    return T
+
+
+@pytest.mark.parametrize("header", sorted(glob.glob(os.path.join(ROOT, "include", "*.h"))),
+                         ids=os.path.basename)
+def test_every_declared_symbol_is_exported(header):
+    lib = ctypes.CDLL(B.lib_path(HEADER_LIBS[os.path.basename(header)]))
+    names = declared_functions(header)
+    assert names
+    for name in names:
+        assert hasattr(lib, name), f"{name} declared in {os.path.basename(header)} but not exported"
+
+
+def test_version_and_status_strings(tc):
+    assert tc.tc_abi_version() == 1
+    lib = tc._lib
+    for code, name in enumerate(["TC_OK", "TC_ERR_INVALID_ARG", "TC_ERR_UNSUPPORTED",
+                                 "TC_ERR_WORKSPACE", "TC_ERR_HIP"]):
+        assert lib.tc_status_string(code).decode() == name
+    assert lib.tc_status_string(99).decode() == "TC_ERR_UNKNOWN"
+
+
+def test_workspace_bytes(tc):
+    lib = tc._lib
+    assert lib.tc_cast_workspace_bytes(-1, 10) == 0
+    sizes = [lib.tc_cast_workspace_bytes(n, 1000) for n in (0, 1, 4096, 4097, 10 ** 6)]
+    assert sizes == sorted(sizes)
+    assert sizes[-1] >= 16 * 10 ** 6   # four int32 arrays of num_pairs
+    assert all(s % 256 == 0 for s in sizes)
+
+
+class HostBuffers:
+    """Host arrays standing in for device buffers: validation must fail
+    before any of them is read or written."""
+
+    def __init__(self):
+        self.f = np.full(4096 + 4, 7.0, dtype=np.float32)
+        self.i = np.full(4096, 7, dtype=np.int32)
+        self.l = np.full(16, 7, dtype=np.int64)
+        self.ws = np.zeros(1 << 16, dtype=np.uint8)
+
+    def fp(self, misalign=False):
+        p = self.f.ctypes.data
+        p = (p + 15) // 16 * 16
+        return p + (4 if misalign else 0)
+
+    def ip(self):
+        return self.i.ctypes.data
+
+    def lp(self):
+        return self.l.ctypes.data
+
+    def wsp(self, misalign=False):
+        p = (self.ws.ctypes.data + 255) // 256 * 256
+        return p + (8 if misalign else 0)
+
+    def untouched(self):
+        return (np.all(self.f == 7.0) and np.all(self.i == 7) and np.all(self.l == 7)
+                and np.all(self.ws == 0))
+
+
+def _err(tc):
+    return tc._lib.tc_last_error().decode()
+
+
+def test_forward_rejects_bad_arguments(tc):
+    lib, h = tc._lib, HostBuffers()
+    f = lambda **k: lib.tc_embed_forward(  # noqa: E731
+        k.get("W", h.fp()), k.get("rows", 100), k.get("dim", 64), k.get("off", h.lp()),
+        k.get("T", 1), k.get("B", 4), k.get("idx", h.ip()), k.get("bo", h.ip()),
+        k.get("out", h.fp()), None)
+    assert f(dim=6) == tc.TC_ERR_UNSUPPORTED and "multiple of 4" in _err(tc)
+    assert f(dim=0) == tc.TC_ERR_UNSUPPORTED
+    assert f(dim=2048) == tc.TC_ERR_UNSUPPORTED
+    assert f(T=-1) == tc.TC_ERR_INVALID_ARG
+    assert f(rows=2 ** 31) == tc.TC_ERR_INVALID_ARG
+    assert f(W=None) == tc.TC_ERR_INVALID_ARG and "null" in _err(tc)
+    assert f(bo=None) == tc.TC_ERR_INVALID_ARG
+    assert f(W=h.fp(misalign=True)) == tc.TC_ERR_UNSUPPORTED
+    assert f(T=0) == tc.TC_OK and _err(tc) == ""          # nothing to do, nothing launched
+    assert h.untouched()
+
+
+def test_cast_rejects_bad_arguments(tc):
+    lib, h = tc._lib, HostBuffers()
+    need = lib.tc_cast_workspace_bytes(1000, 100)
+
+    def f(**k):
+        return lib.tc_cast_index(
+            k.get("off", h.lp()), k.get("T", 1), k.get("B", 50), k.get("rows", 100),
+            k.get("idx", h.ip()), k.get("bo", h.ip()), k.get("n", 1000), k.get("ur", h.ip()),
+            k.get("so", h.ip()), k.get("cs", h.ip()), k.get("cd", None), k.get("nu", h.ip()),
+            k.get("ws", h.wsp()), k.get("wsb", need), None)
+    assert f(wsb=need - 1) == tc.TC_ERR_WORKSPACE and "workspace" in _err(tc)
+    assert f(ws=None) == tc.TC_ERR_WORKSPACE
+    assert f(ws=h.wsp(misalign=True)) == tc.TC_ERR_WORKSPACE
+    assert f(n=-5) == tc.TC_ERR_INVALID_ARG
+    assert f(n=2 ** 31) == tc.TC_ERR_INVALID_ARG
+    assert f(rows=2 ** 31) == tc.TC_ERR_INVALID_ARG
+    assert f(cs=None) == tc.TC_ERR_INVALID_ARG
+    assert f(ur=None) == tc.TC_ERR_INVALID_ARG
+    assert f(nu=None) == tc.TC_ERR_INVALID_ARG
+    assert f(T=0) == tc.TC_ERR_INVALID_ARG     # pairs but no bags
+    assert h.untouched()
+
+
+def test_backward_and_update_reject_bad_arguments(tc):
+    lib, h = tc._lib, HostBuffers()
+
+    def bwd(**k):
+        return lib.tc_embed_backward(k.get("g", h.fp()), k.get("nb", 10), k.get("dim", 8),
+                                     k.get("so", h.ip()), k.get("cs", h.ip()), k.get("nu", h.ip()),
+                                     k.get("mu", 10), k.get("coal", h.fp()), None)
+    assert bwd(dim=10) == tc.TC_ERR_UNSUPPORTED
+    assert bwd(mu=-1) == tc.TC_ERR_INVALID_ARG
+    assert bwd(nu=None) == tc.TC_ERR_INVALID_ARG
+    assert bwd(coal=h.fp(misalign=True)) == tc.TC_ERR_UNSUPPORTED
+    assert bwd(mu=0) == tc.TC_OK
+
+    def upd(**k):
+        return lib.tc_sparse_update(k.get("W", h.fp()), k.get("A", None), k.get("rows", 100),
+                                    k.get("dim", 8), k.get("ur", h.ip()), k.get("coal", h.fp()),
+                                    k.get("nu", h.ip()), k.get("mu", 10), k.get("opt", 0),
+                                    0.01, 1e-8, None)
+    assert upd(A=h.fp()) == tc.TC_ERR_INVALID_ARG               # SGD takes no state
+    assert upd(opt=1) == tc.TC_ERR_INVALID_ARG                  # Adagrad needs state
+    assert upd(opt=7) == tc.TC_ERR_INVALID_ARG
+    assert upd(dim=3) == tc.TC_ERR_UNSUPPORTED
+    assert upd(ur=None) == tc.TC_ERR_INVALID_ARG
+    assert upd(opt=1, A=h.fp(misalign=True)) == tc.TC_ERR_UNSUPPORTED
+    assert h.untouched()
+
+
+def test_launch_without_device_reports_hip_error(tc):
+    """With valid arguments but no GPU, the launch fails and is reported as
+    TC_ERR_HIP with the runtime's message (the kernel never runs)."""
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present; this checks the no-device path only")
+    lib, h = tc._lib, HostBuffers()
+    st = lib.tc_embed_forward(h.fp(), 100, 8, h.lp(), 1, 4, h.ip(), h.ip(), h.fp(), None)
+    assert st == tc.TC_ERR_HIP
+    assert "k_gather_reduce" in _err(tc)
+    assert h.untouched()
