@@ -83,6 +83,7 @@ typedef enum tc_opt_kind {
  * W[table_row_offset[g / bags_per_table] + indices[j], :], starting from +0.
  * An empty bag gives a row of zeros.
  *   W        [total_rows x dim] fp32 table (read only)
+ *   indices  may be NULL when every bag is empty
  *   out      [num_tables*bags_per_table x dim] fp32 (written)
  */
 tc_status tc_embed_forward(const float *W, int64_t total_rows, int32_t dim,

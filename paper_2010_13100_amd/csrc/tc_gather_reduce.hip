@@ -148,7 +148,9 @@ extern "C" tc_status tc_embed_forward(const float *W, int64_t total_rows, int32_
     TC_REQUIRE(dim > 0 && dim % 4 == 0 && dim <= kMaxDim, TC_ERR_UNSUPPORTED,
                "tc_embed_forward: dim %d must be a multiple of 4 in [4, %d]", dim, kMaxDim);
     if (num_bags == 0) return TC_OK;
-    TC_REQUIRE(W && table_row_offset && indices && bag_offsets && out, TC_ERR_INVALID_ARG,
+    // indices is only read for bags that have pairs, so it may be NULL for an
+    // empty index array
+    TC_REQUIRE(W && table_row_offset && bag_offsets && out, TC_ERR_INVALID_ARG,
                "tc_embed_forward: null pointer");
     TC_REQUIRE(aligned16(W) && aligned16(out), TC_ERR_UNSUPPORTED,
                "tc_embed_forward: W and out must be 16-byte aligned");

@@ -16,10 +16,10 @@ TOL = 1e-5  # max relative error of fp32 outputs, row-normwise
 
 def rel_err_rows(got: np.ndarray, ref: np.ndarray) -> float:
     """max over rows of max_d |got - ref| / max_d |ref| (0/0 counts as 0)."""
+    if len(ref) == 0 or np.asarray(ref).size == 0:
+        return 0.0
     got = np.asarray(got, np.float64).reshape(len(ref), -1)
     ref = np.asarray(ref, np.float64).reshape(len(ref), -1)
-    if ref.size == 0:
-        return 0.0
     num = np.abs(got - ref).max(axis=1)
     den = np.abs(ref).max(axis=1)
     r = np.where(den > 0, num / np.where(den > 0, den, 1.0), np.where(num > 0, np.inf, 0.0))
