@@ -25,7 +25,8 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", "-shared", "-ffp-contract=off",
          "-Wall", "-I" + INCLUDE, "-I" + CSRC]
 
 LIBS = {
-    "libtc.so": ["tc_api.hip", "tc_gather_reduce.hip", "tc_cast.hip", "tc_update.hip"],
+    "libtc.so": ["tc_api.hip", "tc_gather_reduce.hip", "tc_backward.hip", "tc_cast.hip",
+                 "tc_update.hip"],
     "libtc_workload.so": ["workload_fill.hip"],
 }
 

@@ -165,5 +165,5 @@ def test_launch_without_device_reports_hip_error(tc):
     lib, h = tc._lib, HostBuffers()
     st = lib.tc_embed_forward(h.fp(), 100, 8, h.lp(), 1, 4, h.ip(), h.ip(), h.fp(), None)
     assert st == tc.TC_ERR_HIP
-    assert "k_gather_reduce" in _err(tc)
+    assert "k_forward" in _err(tc)
     assert h.untouched()
