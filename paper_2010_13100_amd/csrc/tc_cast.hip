@@ -9,7 +9,8 @@
 //       k_radix_scatter stable scatter: a wave ranks equal digits among its
 //                       64 lanes with kRadixBits ballots + popcount, keeps a
 //                       running per-digit count per wave in LDS, and waves
-//                       are combined in tile order.
+//                       are combined in tile order; the tile is laid out in
+//                       sorted order in LDS and stored in that order.
 //     A pass reads and writes 8 bytes per pair plus a 4-byte read for the
 //     histogram. The last pass writes the values straight into casted_src.
 //  3. Segment build (the scan and cumulative sum of Algorithm 2):
@@ -135,22 +136,30 @@ __global__ __launch_bounds__(kBlock) void k_radix_scan(int32_t *__restrict__ cou
     if (threadIdx.x == 0) totals[blockIdx.x] = carry;
 }
 
-// 2c. stable scatter of one tile.
+// 2c. stable scatter of one tile. Ranks are computed as described at the
+// top; the tile is then laid out in sorted order in LDS and written back
+// thread by thread in that order, so neighbouring threads write
+// neighbouring addresses of the same digit run (coalesced stores instead of
+// one scattered store per pair).
 __global__ __launch_bounds__(kBlock) void k_radix_scatter(
     const int32_t *__restrict__ keys_in, const int32_t *__restrict__ vals_in,
     int32_t *__restrict__ keys_out, int32_t *__restrict__ vals_out, int64_t n, int shift,
     int bits, const int32_t *__restrict__ counts, const int32_t *__restrict__ totals,
     int32_t num_tiles) {
     __shared__ int32_t wcount[kSortWaves][kRadix];  // running, then exclusive over waves
-    __shared__ int32_t tile_base[kRadix];           // first output position per digit
+    __shared__ int32_t local_start[kRadix];          // first tile-local position per digit
+    __shared__ int32_t run_shift[kRadix];            // global position - local position
+    __shared__ int32_t stage_key[kTile];
+    __shared__ int32_t stage_val[kTile];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
     const uint32_t mask = (1u << bits) - 1u;
 
     for (int i = tid; i < kSortWaves * kRadix; i += kBlock) (&wcount[0][0])[i] = 0;
+    int32_t tile_base;  // global start of this tile's run of digit `tid`
     {
         int32_t tot;
         const int32_t digit_base = block_exclusive_scan(totals[tid], &tot);
-        tile_base[tid] = digit_base + counts[int64_t(tid) * num_tiles + blockIdx.x];
+        tile_base = digit_base + counts[int64_t(tid) * num_tiles + blockIdx.x];
     }
     __syncthreads();
 
@@ -180,6 +189,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
     }
     __syncthreads();
     {
+        // per digit: exclusive prefix over waves, then over digits
         int32_t s = 0;
 #pragma unroll
         for (int ww = 0; ww < kSortWaves; ++ww) {
@@ -187,6 +197,10 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
             wcount[ww][tid] = s;
             s += c;
         }
+        int32_t tot;
+        const int32_t start = block_exclusive_scan(s, &tot);
+        local_start[tid] = start;
+        run_shift[tid] = tile_base - start;
     }
     __syncthreads();
 #pragma unroll
@@ -194,9 +208,23 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
         const int64_t j = base + i * kWave + lane;
         if (j < n) {
             const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
-            const int32_t pos = tile_base[d] + wcount[w][d] + rank[i];
-            keys_out[pos] = key[i];
-            vals_out[pos] = val[i];
+            const int32_t lp = local_start[d] + wcount[w][d] + rank[i];
+            stage_key[lp] = key[i];
+            stage_val[lp] = val[i];
+        }
+    }
+    __syncthreads();
+    const int64_t tile0 = int64_t(blockIdx.x) * kTile;
+    const int32_t in_tile = int32_t(n - tile0 < kTile ? n - tile0 : kTile);
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+        const int32_t lp = i * kBlock + tid;
+        if (lp < in_tile) {
+            const int32_t k = stage_key[lp];
+            const uint32_t d = (uint32_t(k) >> shift) & mask;
+            const int32_t pos = run_shift[d] + lp;
+            keys_out[pos] = k;
+            vals_out[pos] = stage_val[lp];
         }
     }
 }
