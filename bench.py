@@ -35,23 +35,27 @@ def algorithmic_bytes(w, n, u, nbags):
     return {"forward": fwd, "cast": cast, "backward": bwd, "update": upd}
 
 
+# Sources of each call's kernels, and the kernels one call launches.
 KERNEL_SOURCES = {
-    "forward": "tc_gather_reduce.hip",
-    "backward": "tc_gather_reduce.hip",
-    "update": "tc_update.hip",
-    "cast": "tc_cast.hip",
+    "forward": ["tc_internal.h", "tc_group_sum.h", "tc_gather_reduce.hip"],
+    "backward": ["tc_internal.h", "tc_group_sum.h", "tc_backward.hip"],
+    "update": ["tc_internal.h", "tc_update.hip"],
+    "cast": ["tc_internal.h", "tc_cast.hip"],
 }
 KERNEL_NAMES = {
-    "forward": "k_gather_reduce (forward)",
-    "backward": "k_gather_reduce (backward)",
-    "update": "k_sparse_update",
-    "cast": "tc_cast_index (9+ kernels)",
+    "forward": ["k_forward"],
+    "backward": ["k_backward_long", "k_backward_short"],
+    "update": ["k_sparse_update"],
+    "cast": ["k_build_keys", "k_radix_hist", "k_radix_scan", "k_radix_scatter", "k_seg_count",
+             "k_seg_scan", "k_seg_write"],
 }
 
 
 def source_sha(call: str) -> str:
-    p = os.path.join(ROOT, "paper_2010_13100_amd", "csrc", KERNEL_SOURCES[call])
-    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[call]:
+        h.update(open(os.path.join(ROOT, "paper_2010_13100_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def load_traffic(call: str, workload: str):
@@ -64,6 +68,65 @@ def load_traffic(call: str, workload: str):
     if not entry or entry.get("source_sha") != source_sha(call):
         return None
     return entry["hbm_bytes_per_launch"]
+
+
+def write_traffic(pmc_dir: str, workload: str) -> dict:
+    """Turn four rocprofv3 --pmc CSV runs into HBM bytes per call launch and
+    store them in profiles/traffic.json under "<call>:<workload>".
+
+    pmc_dir holds copy_fetch/, copy_write/ (bench.py --copy-calibration runs)
+    and fetch/, write/ (runs of this workload), each with the
+    run_counter_collection.csv that `rocprofv3 --pmc FETCH_SIZE|WRITE_SIZE -f csv
+    -o run` writes. FETCH_SIZE and WRITE_SIZE are KiB per dispatch; each is
+    scaled by copy_bytes / counter-reading-for-the-copy, the counter's own error
+    on a plain device copy of known size."""
+    import csv
+    import re
+
+    def rows(sub):
+        with open(os.path.join(pmc_dir, sub, "run_counter_collection.csv")) as f:
+            return list(csv.DictReader(f))
+
+    def per_kernel(sub):
+        out: dict = {}
+        for r in rows(sub):
+            out.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]) * 1024.0)
+        return out
+
+    scale = {}
+    for sub, counter in (("copy_fetch", "FETCH_SIZE"), ("copy_write", "WRITE_SIZE")):
+        copies = [float(r["Counter_Value"]) * 1024.0 for r in rows(sub)
+                  if "copyBuffer" in r["Kernel_Name"]]
+        bytes_per_copy = int(open(os.path.join(pmc_dir, "copy_bytes")).read())
+        scale[counter] = bytes_per_copy / (sum(copies) / len(copies))
+    fetch, write = per_kernel("fetch"), per_kernel("write")
+    p = os.path.join(ROOT, "profiles", "traffic.json")
+    table = json.load(open(p)) if os.path.exists(p) else {}
+    for call, names in KERNEL_NAMES.items():
+        fb = wb = 0.0
+        found = True
+        for k in names:
+            pat = re.compile(r"\b" + k + r"\b")
+            fv = [v for n, vs in fetch.items() if pat.search(n) for v in vs]
+            wv = [v for n, vs in write.items() if pat.search(n) for v in vs]
+            if not fv or not wv:
+                found = False
+                break
+            fb += sum(fv) / len(fv)
+            wb += sum(wv) / len(wv)
+        if not found:
+            continue
+        fb *= scale["FETCH_SIZE"]
+        wb *= scale["WRITE_SIZE"]
+        table[f"{call}:{workload}"] = {
+            "source_sha": source_sha(call), "kernels": names,
+            "fetch_bytes_per_launch": round(fb), "write_bytes_per_launch": round(wb),
+            "hbm_bytes_per_launch": round(fb + wb),
+            "fetch_scale": round(scale["FETCH_SIZE"], 4), "write_scale": round(scale["WRITE_SIZE"], 4)}
+    with open(p, "w") as f:
+        json.dump(table, f, indent=1, sort_keys=True)
+        f.write("\n")
+    return table
 
 
 def cpu_baseline(w, batch, budget_s: float):
@@ -103,7 +166,25 @@ def main():
     ap.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle work for cpu_baseline (0 disables)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run 5 plain device copies of BYTES bytes (scale for the HBM "
+                         "byte counters) and exit")
+    ap.add_argument("--traffic-from", metavar="PMC_DIR", default=None,
+                    help="write profiles/traffic.json entries for --config from rocprofv3 "
+                         "counter runs in PMC_DIR and exit (no GPU needed)")
     args = ap.parse_args()
+    if args.traffic_from:
+        print(json.dumps(write_traffic(args.traffic_from, args.config), indent=1))
+        return
+    if args.copy_calibration:
+        import torch
+        src = torch.ones(args.copy_calibration // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": args.copy_calibration, "copies": 5}))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the hot path is built and timed on a single "
               "MI355X; run with --gpus 1", file=sys.stderr)
@@ -188,6 +269,7 @@ def main():
     dom = max(single, key=lambda c: per_call_ms[c])
     achieved = nbytes[dom] / (per_call_ms[dom] * 1e-3) / 1e9
     traffic = load_traffic(dom, args.config)
+    traffic_gbs = None if traffic is None else traffic / (per_call_ms[dom] * 1e-3) / 1e9
     result = {
         "metric": "embedding train steps/sec (fwd+cast+bwd+update) and achieved HBM GB/s",
         "value": round(args.steps / (ms_total * 1e-3), 3),
@@ -213,10 +295,14 @@ def main():
         "per_call_us": {c: round(v * 1e3, 2) for c, v in per_call_ms.items()},
         "per_call_algorithmic_GBps": {c: round(nbytes[c] / (per_call_ms[c] * 1e-3) / 1e9, 1)
                                       for c in calls},
-        "roofline": {"bound": "hbm", "kernel": KERNEL_NAMES[dom],
+        "roofline": {"bound": "hbm", "call": f"tc_embed_{dom}" if dom != "update"
+                     else "tc_sparse_update", "kernels": KERNEL_NAMES[dom],
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic},
+                     "traffic": traffic,
+                     "traffic_GBps": None if traffic_gbs is None else round(traffic_gbs, 1),
+                     "traffic_frac": None if traffic_gbs is None
+                     else round(traffic_gbs / HBM_PEAK_GBS, 4)},
     }
     if args.cpu_budget > 0:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
