@@ -7,12 +7,12 @@
 // keep the result bitwise equal to the sequential definition. Two kernels
 // split the work by segment length:
 //
-//  k_backward_long   segments of at least kLongSegment pairs. One wavefront
-//                    per (segment, 16-column part); each load instruction
-//                    brings 4 rows of the part into neighbouring lanes, a
-//                    register ring keeps 64 loads (256 rows) in flight, and
-//                    the ordered adds take the rows through DPP row shifts
-//                    (column_chain).
+//  k_backward_long   segments of at least kLongSegment pairs. One workgroup
+//                    per (segment, 64-column part): four producer
+//                    wavefronts gather the rows into a ring of LDS buffers
+//                    with 16-byte loads, and one consumer wavefront (one
+//                    column per lane) runs the ordered adds out of LDS, so
+//                    the chain never waits behind load issue.
 //  k_backward_short  the other segments: lane groups exactly as the forward.
 //
 // The long kernel is launched first; both only read their inputs and write
@@ -26,209 +26,246 @@ namespace {
 
 // Segments at least this long go to k_backward_long.
 constexpr int kLongSegment = 128;
-// Columns per long-chain wavefront, and rows per load instruction: a
-// wavefront issues about one load instruction per 32 cycles, so each load
-// brings 4 rows (of 64 bytes; narrower pieces cost more memory requests).
-constexpr int kChainCols = 16;
-constexpr int kRowsPerLoad = kWave / kChainCols;  // 4
-constexpr int kGroupsPerIdVector = kWave / kRowsPerLoad;  // 16 groups = 64 rows
-// Groups (one load each) a chain keeps in flight: four id blocks.
-constexpr int kRing = 4 * kGroupsPerIdVector;  // 64 loads, 256 rows
-// Blocks of the long kernel; each scans its own range of segments and has up
-// to kMaxLongWaves wavefronts.
-constexpr int kLongBlocks = 1024;
-constexpr int kMaxLongWaves = 8;
+// A long-segment workgroup: one consumer and kProducers producer wavefronts.
+constexpr int kProducers = 4;
+constexpr int kLongThreads = (1 + kProducers) * kWave;
+// Columns per workgroup (one per consumer lane) and rows per LDS buffer.
+constexpr int kPartCols = kWave;
+constexpr int kChunkRows = 64;
+constexpr int kBuffers = 3;
+// A producer load instruction brings kRowsPerLoad rows of the part: 16
+// lanes x 16 bytes per row.
+constexpr int kLanesPerRow = kPartCols / 4;
+constexpr int kRowsPerLoad = kWave / kLanesPerRow;  // 4
+constexpr int kLoadsPerChunk = kChunkRows / kRowsPerLoad;  // 16
+// Chunks whose row loads (kAhead) and id loads (kIdAhead) a producer keeps in
+// flight; the producer code is unrolled over kPeriod chunks so that every ring
+// slot is a fixed register.
+constexpr int kAhead = 6;
+constexpr int kIdAhead = 12;
+constexpr int kPeriod = 12;
+static_assert(kPeriod % kAhead == 0 && kPeriod % kIdAhead == 0 && kPeriod % kBuffers == 0,
+              "ring periods must divide kPeriod");
+// Ranges of segments scanned by the blocks of the long kernel (per part).
+constexpr int kLongRanges = 1024;
 // Buffer resource word 3 for gfx9-family buffers; out-of-range reads give 0.
 constexpr int32_t kBufferWord3 = 0x00020000;
+// A buffer offset past every resource here (resources span < 2^31 bytes):
+// rows past the end of a segment load as +0.0, which leaves the sum unchanged
+// (a sum started at +0.0 is never -0.0, and x + 0.0 == x for every other x).
+constexpr int32_t kOutOfRange = 0x7ffff000;
 
-// Per-wavefront LDS table of the byte offsets of the rows of one block.
-struct ChainLds {
-    int32_t offs[kWave];
+// LDS buffer layout: column-major, so that one 16-byte read gives a consumer
+// lane four consecutive rows of its column. Within column c, the group of
+// rows 4k..4k+3 sits at group position k ^ swz(c); the swizzle spreads both
+// the consumer's 16-byte reads (16 neighbouring columns, same k) and the
+// producers' 4-byte writes (16 columns 4 apart, same k) over distinct banks.
+struct LongLds {
+    alignas(16) float cols[kBuffers][kPartCols][kChunkRows];
+    int32_t offs[kProducers][kChunkRows];
 };
+__device__ __forceinline__ int32_t swz(int32_t c) { return (c & 15) ^ ((c >> 4) & 3); }
+// byte offset of (row r, column c) within one buffer
+__device__ __forceinline__ int32_t lds_pos(int32_t r, int32_t c) {
+    return (c * kChunkRows + 4 * ((r >> 2) ^ swz(c)) + (r & 3)) * 4;
+}
+constexpr int32_t kBufferBytes = kPartCols * kChunkRows * 4;
 
-// v of the lane K places up within each row of 16 lanes (DPP row_shl:K).
-// All 64 lanes are active wherever this is used, and the lanes that keep the
-// result read within their row, so the bound_ctrl setting (which lets the
-// compiler fold the move into the add) never changes a kept value.
+// Workgroup barrier that orders LDS only: outstanding global loads stay in
+// flight across it.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 template <int K>
-__device__ __forceinline__ float lane_up(float v) {
-    return __builtin_bit_cast(
-        float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x100 + K, 0xf, 0xf, true));
-}
+using Int = std::integral_constant<int, K>;
 
-// acc + the lane's group of kRowsPerLoad rows (its own value, then those of
-// the next lanes), in order.
-__device__ __forceinline__ float add_group(float acc, float x) {
-    acc = acc + x;
-    acc = acc + lane_up<1>(x);
-    acc = acc + lane_up<2>(x);
-    acc = acc + lane_up<3>(x);
-    return acc;
-}
-// The same for only the first n rows of the group.
-__device__ __forceinline__ float add_group_partial(float acc, float x, int32_t n) {
-    if (n > 0) acc = acc + x;
-    if (n > 1) acc = acc + lane_up<1>(x);
-    if (n > 2) acc = acc + lane_up<2>(x);
-    if (n > 3) acc = acc + lane_up<3>(x);
-    return acc;
-}
-static_assert(kRowsPerLoad == 4, "add_group adds four rows");
-
-// One wavefront sums rows ids[beg..end) of grad for the kChainCols columns
-// [q0, q0+16) in order. Lane l reads column q0 + l/4 of row 4g + l%4 of
-// group g, so one dword load brings 4 rows (64 bytes each) and the four rows
-// of a column sit in four neighbouring lanes; lane 4c adds them in order
-// through DPP row shifts, which need no LDS and fold into the adds.
-// Loads are buffer loads (row byte offset + lane column offset) against a
-// resource spanning the segment's rows, whose ids are sorted; ids are read
-// 64 at a time (one per lane, positions clamped into the segment) eight id
-// blocks ahead of use, so waiting for them never drains the ring, and a
-// block's row offsets pass through a small LDS table. The ring holds kRing
-// loads (256 rows); the slot of group g is g % kRing, refilled with group
-// g + kRing right after it is consumed. Scheduling barriers every 4 groups
-// keep loads and adds from being regrouped. Rows past the end are skipped.
-__device__ void column_chain(ChainLds &lds, const float *__restrict__ grad, int32_t dim,
-                              const int32_t *__restrict__ ids, int32_t beg, int32_t end,
-                              int32_t q0, float *__restrict__ out_row) {
+// Producer P of a long segment (rows ids[0..len) of grad, part columns at
+// byte offset part_bytes). It gathers chunk c (rows 64c..64c+63) with the
+// load instructions k = P, P + kProducers, ... of the chunk; instruction k brings rows
+// 4k..4k+3, lane l reading 16 bytes of row 4k + l/16. Chunk c's loads are
+// issued kAhead chunks before it is written to LDS buffer c % 3, two chunks
+// ahead of the consumer; the chunk's ids are loaded kIdAhead chunks before
+// that and turned into row offsets through a small per-producer LDS table.
+// Executes exactly 1 + nchunks barriers, as the consumer does.
+template <int P>
+__device__ void long_producer(LongLds &lds, __amdgpu_buffer_rsrc_t id_rsrc, int32_t len,
+                              int32_t first, int32_t row_bytes, int32_t part_bytes,
+                              int32_t nchunks, __amdgpu_buffer_rsrc_t rsrc) {
+    constexpr int L = (kLoadsPerChunk - P + kProducers - 1) / kProducers;
     const int lane = threadIdx.x & (kWave - 1);
-    const int row_sel = lane & (kRowsPerLoad - 1);
-    const int32_t col = q0 + lane / kRowsPerLoad;
-    const int32_t rcol = col < dim ? col : dim - 1;  // column this lane reads
-    const int32_t len = end - beg;
-    const int32_t *sid = ids + beg;
-    const int32_t first = __builtin_amdgcn_readfirstlane(sid[0]);
-    const int32_t last = __builtin_amdgcn_readfirstlane(sid[len - 1]);
-    const int32_t row_bytes = dim * 4;
-    const uint64_t span = uint64_t(last - first + 1) * uint64_t(row_bytes);
-    const bool writer = row_sel == 0 && col < dim;
-    if (span >= (uint64_t(1) << 31)) {
-        // rows spread over 2 GiB or more: plain 64-bit addressed loads
-        float acc = 0.f;
-        const float *colp = grad + rcol;
-        for (int32_t k = 0; k < len; ++k) acc = acc + colp[int64_t(sid[k]) * dim];
-        if (writer) out_row[col] = acc;
-        return;
-    }
-    const auto rsrc = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<float *>(grad + int64_t(first) * dim), 0, int32_t(span), kBufferWord3);
-    const int32_t lane_bytes = rcol * 4;
-    // ids of block k (rows 64k..64k+63), one per lane; positions clamped into
-    // the segment
-    auto load_ids = [&](int32_t k) -> int32_t { return sid[min(k * kWave + lane, len - 1)]; };
-    auto set_offsets = [&](int32_t idv) { lds.offs[lane] = (idv - first) * row_bytes; };
-    auto group_offset = [&](int gi) -> int32_t { return lds.offs[gi * kRowsPerLoad + row_sel]; };
-    auto load_group = [&](int32_t off) -> float {
-        return __builtin_bit_cast(
-            float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, off + lane_bytes, 0, 0));
+    const int rsel = lane / kLanesPerRow;
+    const int32_t col4 = (lane % kLanesPerRow) * 4;  // first of the lane's 4 columns
+    const int32_t lane_bytes = part_bytes + col4 * 4;
+    int32_t *offs = lds.offs[P];
+    // ids of chunk c, one per lane (0 past the end of the segment; such rows
+    // get kOutOfRange below)
+    auto load_ids = [&](int32_t c) -> int32_t {
+        return __builtin_amdgcn_raw_buffer_load_b32(id_rsrc, lane * 4, c * (kChunkRows * 4), 0);
     };
-
-    // Block B's ids live in iv[B % 8] from 8 blocks before the block that
-    // uses them (block B-4 refills the ring with block B). Issue every id load
-    // of blocks 0..11 before the first row load.
-    int32_t iv[8];
-    const int32_t p0 = load_ids(0), p1 = load_ids(1), p2 = load_ids(2), p3 = load_ids(3);
+    int32_t iv[kIdAhead];
+    float4 d[kAhead][L];
+    auto issue = [&](auto ds, auto es, int32_t c) {
+        constexpr int DS = decltype(ds)::value, ES = decltype(es)::value;
+        offs[lane] = c * kChunkRows + lane < len ? (iv[ES] - first) * row_bytes : kOutOfRange;
+        int32_t o[L];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) iv[k] = load_ids(k < 4 ? k + 8 : k);
-    float ring[kRing];
-    {
-        const int32_t pk[4] = {p0, p1, p2, p3};
+        for (int t = 0; t < L; ++t) o[t] = offs[(P + kProducers * t) * kRowsPerLoad + rsel];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            set_offsets(pk[k]);
-#pragma unroll
-            for (int gi = 0; gi < kGroupsPerIdVector; ++gi)
-                ring[k * kGroupsPerIdVector + gi] = load_group(group_offset(gi));
-        }
-    }
-
-    float acc = 0.f;
-    // A full block blk (64 rows; B = blk % 8 at compile time): consume its
-    // ring slots (those of blk % 4) and refill them with block blk + 4.
-    auto full_block = [&](auto bconst, int32_t blk) {
-        constexpr int B = decltype(bconst)::value;
-        set_offsets(iv[(B + 4) % 8]);
-        int32_t offs[kGroupsPerIdVector];
-#pragma unroll
-        for (int gi = 0; gi < kGroupsPerIdVector; ++gi) offs[gi] = group_offset(gi);
-#pragma unroll
-        for (int gi = 0; gi < kGroupsPerIdVector; ++gi) {
-            const int slot = (B % 4) * kGroupsPerIdVector + gi;
-            acc = add_group(acc, ring[slot]);
-            ring[slot] = load_group(offs[gi]);
-            if (gi % 4 == 3) __builtin_amdgcn_sched_barrier(0);
-        }
-        iv[(B + 4) % 8] = load_ids(blk + 12);
+        for (int t = 0; t < L; ++t)
+            d[DS][t] = __builtin_bit_cast(
+                float4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, o[t] + lane_bytes, 0, 0));
+        iv[ES] = load_ids(c + kIdAhead);
     };
-    // The partial last block (fewer than 64 rows left; Q = blk % 4).
-    auto last_block = [&](auto qconst, int32_t rows_left) {
-        constexpr int Q = decltype(qconst)::value;
+    // byte offsets of this lane's four columns of row 4k + rsel, k = P + 3t
+    int32_t wpos[L][4];
 #pragma unroll
-        for (int gi = 0; gi < kGroupsPerIdVector; ++gi) {
-            acc = add_group_partial(acc, ring[Q * kGroupsPerIdVector + gi],
-                                    rows_left - gi * kRowsPerLoad);
+    for (int t = 0; t < L; ++t)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            wpos[t][e] = lds_pos((P + kProducers * t) * kRowsPerLoad + rsel, col4 + e);
+    char *lds_cols = reinterpret_cast<char *>(&lds.cols[0][0][0]);
+    auto write = [&](auto ds, auto bs) {
+        constexpr int DS = decltype(ds)::value, B = decltype(bs)::value;
+#pragma unroll
+        for (int t = 0; t < L; ++t) {
+            const float4 v = d[DS][t];
+            *reinterpret_cast<float *>(lds_cols + B * kBufferBytes + wpos[t][0]) = v.x;
+            *reinterpret_cast<float *>(lds_cols + B * kBufferBytes + wpos[t][1]) = v.y;
+            *reinterpret_cast<float *>(lds_cols + B * kBufferBytes + wpos[t][2]) = v.z;
+            *reinterpret_cast<float *>(lds_cols + B * kBufferBytes + wpos[t][3]) = v.w;
         }
     };
-    using I0 = std::integral_constant<int, 0>;
-    using I1 = std::integral_constant<int, 1>;
-    using I2 = std::integral_constant<int, 2>;
-    using I3 = std::integral_constant<int, 3>;
-    using I4 = std::integral_constant<int, 4>;
-    using I5 = std::integral_constant<int, 5>;
-    using I6 = std::integral_constant<int, 6>;
-    using I7 = std::integral_constant<int, 7>;
-    // Only full blocks run in the loop, and it is left by early exits, so
-    // no partial path joins the steady state (which would make the compiler
-    // wait for every outstanding load).
-    int32_t blk = 0;
-    for (;;) {
-        if (len - blk * kWave < kWave) break;
-        full_block(I0{}, blk++);
-        if (len - blk * kWave < kWave) break;
-        full_block(I1{}, blk++);
-        if (len - blk * kWave < kWave) break;
-        full_block(I2{}, blk++);
-        if (len - blk * kWave < kWave) break;
-        full_block(I3{}, blk++);
-        if (len - blk * kWave < kWave) break;
-        full_block(I4{}, blk++);
-        if (len - blk * kWave < kWave) break;
-        full_block(I5{}, blk++);
-        if (len - blk * kWave < kWave) break;
-        full_block(I6{}, blk++);
-        if (len - blk * kWave < kWave) break;
-        full_block(I7{}, blk++);
+#pragma unroll
+    for (int e = 0; e < kIdAhead; ++e) iv[e] = load_ids(e);
+    static_assert(kAhead == 6, "the prologue issues kAhead chunks");
+    issue(Int<0>{}, Int<0>{}, 0);
+    issue(Int<1>{}, Int<1>{}, 1);
+    issue(Int<2>{}, Int<2>{}, 2);
+    issue(Int<3>{}, Int<3>{}, 3);
+    issue(Int<4>{}, Int<4>{}, 4);
+    issue(Int<5>{}, Int<5>{}, 5);
+    write(Int<0>{}, Int<0>{});
+    issue(Int<0>{}, Int<6>{}, 6);
+    write(Int<1>{}, Int<1>{});
+    issue(Int<1>{}, Int<7>{}, 7);
+    lds_barrier();
+    // Step i: write chunk i + 2, refill its registers with chunk i + 2 + kAhead.
+    auto step = [&](auto ms, int32_t i) {
+        constexpr int M = decltype(ms)::value;  // i % kPeriod
+        write(Int<(M + 2) % kAhead>{}, Int<(M + 2) % kBuffers>{});
+        issue(Int<(M + 2) % kAhead>{}, Int<(M + 2 + kAhead) % kIdAhead>{}, i + 2 + kAhead);
+        lds_barrier();
+    };
+    // Whole periods in a loop with a single exit (a loop left from the middle
+    // merges the load bookkeeping of every exit at its head, which costs a
+    // full wait), then the remaining steps once.
+    static_assert(kPeriod == 12, "the step loop is unrolled over 12 chunks");
+    int32_t i = 0;
+    const int32_t periods = nchunks / kPeriod;
+    for (int32_t k = 0; k < periods; ++k, i += kPeriod) {
+        step(Int<0>{}, i);
+        step(Int<1>{}, i + 1);
+        step(Int<2>{}, i + 2);
+        step(Int<3>{}, i + 3);
+        step(Int<4>{}, i + 4);
+        step(Int<5>{}, i + 5);
+        step(Int<6>{}, i + 6);
+        step(Int<7>{}, i + 7);
+        step(Int<8>{}, i + 8);
+        step(Int<9>{}, i + 9);
+        step(Int<10>{}, i + 10);
+        step(Int<11>{}, i + 11);
     }
-    const int32_t rows_left = len - blk * kWave;
-    if (rows_left > 0) {
-        switch (blk % 4) {
-            case 0: last_block(I0{}, rows_left); break;
-            case 1: last_block(I1{}, rows_left); break;
-            case 2: last_block(I2{}, rows_left); break;
-            default: last_block(I3{}, rows_left); break;
-        }
-    }
-    if (writer) out_row[col] = acc;
+    const int32_t rem = nchunks - i;
+    if (rem > 0) { step(Int<0>{}, i);
+    if (rem > 1) { step(Int<1>{}, i + 1);
+    if (rem > 2) { step(Int<2>{}, i + 2);
+    if (rem > 3) { step(Int<3>{}, i + 3);
+    if (rem > 4) { step(Int<4>{}, i + 4);
+    if (rem > 5) { step(Int<5>{}, i + 5);
+    if (rem > 6) { step(Int<6>{}, i + 6);
+    if (rem > 7) { step(Int<7>{}, i + 7);
+    if (rem > 8) { step(Int<8>{}, i + 8);
+    if (rem > 9) { step(Int<9>{}, i + 9);
+    if (rem > 10) { step(Int<10>{}, i + 10);
+    }}}}}}}}}}}
 }
 
-// Each block scans a contiguous range of segments; its wavefronts split the
-// 16-column parts of every long segment found. A first pass reads every
-// 64th offset: a batch of 64 segments spanning fewer than kLongSegment pairs
-// cannot hold a long one and is skipped without reading its offsets.
-__global__ __launch_bounds__(512) void k_backward_long(
+// The consumer: lane l owns column l of the part and adds the rows of chunk
+// i in order, 64 per step, four rows per 16-byte LDS read. Chunk i + 1 is
+// complete in LDS during step i (it was written one step ahead), so step i
+// reads it into registers between the adds of chunk i and the chain never
+// waits for LDS. Executes exactly 1 + nchunks barriers, as the producers do.
+__device__ float long_consumer(LongLds &lds, int32_t nchunks) {
+    constexpr int G = kChunkRows / 4;
+    const int lane = threadIdx.x & (kWave - 1);
+    const char *lds_cols = reinterpret_cast<const char *>(&lds.cols[0][0][0]);
+    int32_t rpos[G];  // byte offset of rows 4k..4k+3 of this lane's column
+#pragma unroll
+    for (int k = 0; k < G; ++k) rpos[k] = lds_pos(4 * k, lane);
+    float acc = 0.f;
+    lds_barrier();
+    float4 xa[G], xb[G];
+#pragma unroll
+    for (int k = 0; k < G; ++k) xa[k] = *reinterpret_cast<const float4 *>(lds_cols + rpos[k]);
+    // adds cur (chunk i) while reading chunk i + 1 from buffer B into nxt
+    auto step = [&](auto bs, const float4(&cur)[G], float4(&nxt)[G]) {
+        constexpr int B = decltype(bs)::value;
+#pragma unroll
+        for (int k = 0; k < G; ++k) {
+            nxt[k] = *reinterpret_cast<const float4 *>(lds_cols + B * kBufferBytes + rpos[k]);
+            acc = acc + cur[k].x;
+            acc = acc + cur[k].y;
+            acc = acc + cur[k].z;
+            acc = acc + cur[k].w;
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        lds_barrier();
+    };
+    // step i reads buffer (i + 1) % 3 into the other register set: period 6
+    int32_t i = 0;
+    for (;;) {
+        if (i >= nchunks) break;
+        step(Int<1>{}, xa, xb);
+        if (++i >= nchunks) break;
+        step(Int<2>{}, xb, xa);
+        if (++i >= nchunks) break;
+        step(Int<0>{}, xa, xb);
+        if (++i >= nchunks) break;
+        step(Int<1>{}, xb, xa);
+        if (++i >= nchunks) break;
+        step(Int<2>{}, xa, xb);
+        if (++i >= nchunks) break;
+        step(Int<0>{}, xb, xa);
+        ++i;
+    }
+    return acc;
+}
+
+// Each block (range x, part y) scans a contiguous range of segments and runs
+// every long one it finds for its part. All four wavefronts scan the same
+// offsets, so they agree on every segment and on its number of chunks, which
+// fixes the barrier count. A first pass reads every 64th offset: a batch of
+// 64 segments spanning fewer than kLongSegment pairs cannot hold a long one.
+__global__ __launch_bounds__(kLongThreads) void k_backward_long(
     const float *__restrict__ grad, int32_t dim, const int32_t *__restrict__ ids,
     const int32_t *__restrict__ offsets, const int32_t *__restrict__ num_out_dev,
     int64_t num_out_cap, float *__restrict__ out) {
-    __shared__ ChainLds chain_lds[kMaxLongWaves];
+    __shared__ LongLds lds;
     const int lane = threadIdx.x & (kWave - 1);
-    const int w = threadIdx.x / kWave;
-    const int nw = blockDim.x / kWave;
-    const int32_t parts = (dim + kChainCols - 1) / kChainCols;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int32_t part = blockIdx.y;
+    const int32_t col = part * kPartCols + lane;
+    const int32_t row_bytes = dim * 4;
     const int64_t u_dev = *num_out_dev;
     const int64_t num = u_dev < num_out_cap ? u_dev : num_out_cap;
     const int64_t per = (num + gridDim.x - 1) / gridDim.x;
     const int64_t r0 = int64_t(blockIdx.x) * per;
     const int64_t r1 = r0 + per < num ? r0 + per : num;
+    if (w == 0) __builtin_amdgcn_s_setprio(3);
     for (int64_t c0 = r0; c0 < r1; c0 += int64_t(kWave) * kWave) {
         const int64_t s0 = c0 + int64_t(kWave) * lane;  // this lane's batch
         const int32_t os = offsets[s0 < r1 ? s0 : r1];
@@ -248,12 +285,47 @@ __global__ __launch_bounds__(512) void k_backward_long(
             while (longs) {
                 const int j = __builtin_ctzll(longs);
                 longs &= longs - 1;
-                const int32_t b = __builtin_amdgcn_readlane(o0, j);
-                const int32_t e = __builtin_amdgcn_readlane(o1, j);
+                const int32_t beg = __builtin_amdgcn_readlane(o0, j);
+                const int32_t len = __builtin_amdgcn_readlane(o1, j) - beg;
                 const int64_t seg = c0 + int64_t(kWave) * i + j;
-                for (int32_t q = w; q < parts; q += nw)
-                    column_chain(chain_lds[w], grad, dim, ids, b, e, q * kChainCols,
-                                 out + seg * int64_t(dim));
+                float *out_row = out + seg * int64_t(dim);
+                const int32_t *sid = ids + beg;
+                // ids within a segment are non-decreasing (stable cast order)
+                const int32_t first = __builtin_amdgcn_readfirstlane(sid[0]);
+                const int32_t last = __builtin_amdgcn_readfirstlane(sid[len - 1]);
+                const uint64_t span = uint64_t(last - first + 1) * uint64_t(row_bytes);
+                if (span >= (uint64_t(1) << 31) || len >= (1 << 29)) {
+                    // rows spread over 2 GiB or more (or a segment too long for
+                    // 32-bit byte offsets of its ids): the consumer alone, with
+                    // 64-bit addressed loads (no barriers on this path)
+                    if (w == 0) {
+                        float acc = 0.f;
+                        const float *colp = grad + (col < dim ? col : dim - 1);
+                        for (int32_t k = 0; k < len; ++k)
+                            acc = acc + colp[int64_t(sid[k]) * dim];
+                        if (col < dim) out_row[col] = acc;
+                    }
+                    continue;
+                }
+                const int32_t nchunks = (len + kChunkRows - 1) / kChunkRows;
+                const auto id_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+                    const_cast<int32_t *>(sid), 0, len * 4, kBufferWord3);
+                const auto rsrc = __builtin_amdgcn_make_buffer_rsrc(
+                    const_cast<float *>(grad + int64_t(first) * dim), 0, int32_t(span),
+                    kBufferWord3);
+                const int32_t part_bytes = part * kPartCols * 4;
+                if (w == 0) {
+                    const float acc = long_consumer(lds, nchunks);
+                    if (col < dim) out_row[col] = acc;
+                } else if (w == 1) {
+                    long_producer<0>(lds, id_rsrc, len, first, row_bytes, part_bytes, nchunks, rsrc);
+                } else if (w == 2) {
+                    long_producer<1>(lds, id_rsrc, len, first, row_bytes, part_bytes, nchunks, rsrc);
+                } else if (w == 3) {
+                    long_producer<2>(lds, id_rsrc, len, first, row_bytes, part_bytes, nchunks, rsrc);
+                } else {
+                    long_producer<3>(lds, id_rsrc, len, first, row_bytes, part_bytes, nchunks, rsrc);
+                }
             }
         }
     }
@@ -295,10 +367,10 @@ __global__ __launch_bounds__(kBlock) void k_backward_short(
 tc_status launch_backward(const float *grad, int32_t dim, const int32_t *ids,
                           const int32_t *offsets, const int32_t *num_out_dev, int64_t cap,
                           float *out, hipStream_t stream) {
-    const int parts = (dim + kChainCols - 1) / kChainCols;
-    const int long_waves = parts < kMaxLongWaves ? parts : kMaxLongWaves;
-    k_backward_long<<<kLongBlocks, long_waves * kWave, 0, stream>>>(grad, dim, ids, offsets,
-                                                                     num_out_dev, cap, out);
+    const int parts = (dim + kPartCols - 1) / kPartCols;
+    const int ranges = kLongRanges / parts > 64 ? kLongRanges / parts : 64;
+    k_backward_long<<<dim3(ranges, parts), kLongThreads, 0, stream>>>(grad, dim, ids, offsets,
+                                                                       num_out_dev, cap, out);
     tc_status st = check_launch("k_backward_long");
     if (st != TC_OK) return st;
     const RowShape s = row_shape(dim);
