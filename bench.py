@@ -162,7 +162,7 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle work for cpu_baseline (0 disables)")
@@ -212,43 +212,55 @@ def main():
                  grad=torch.from_numpy(b.grad_out).to(dev), n=b.num_pairs) for b in batches]
     stream = torch.cuda.current_stream(dev)
 
+    calls = ["forward", "cast", "backward", "update"]
+    fns = {"forward": lambda d: trainer.forward(d["off"], d["idx"], d["bo"], stream),
+           "cast": lambda d: trainer.cast(d["off"], d["idx"], d["bo"], d["n"], stream),
+           "backward": lambda d: trainer.backward(d["grad"], stream),
+           "update": lambda d: trainer.update(stream)}
+
     def step(i, ev=None):
+        """One step on batch i % NUM_BATCHES. ev: dict call -> (start, stop)
+        events to record around that call (each record is a marker on the
+        stream, so the timed steps record only the dominant call's pair)."""
         d = dbat[i % NUM_BATCHES]
-        if ev is not None:
-            ev[0].record(stream)
-        trainer.forward(d["off"], d["idx"], d["bo"], stream)
-        if ev is not None:
-            ev[1].record(stream)
-        trainer.cast(d["off"], d["idx"], d["bo"], d["n"], stream)
-        if ev is not None:
-            ev[2].record(stream)
-        trainer.backward(d["grad"], stream)
-        if ev is not None:
-            ev[3].record(stream)
-        trainer.update(stream)
-        if ev is not None:
-            ev[4].record(stream)
+        for c in calls:
+            e = ev.get(c) if ev else None
+            if e:
+                e[0].record(stream)
+            fns[c](d)
+            if e:
+                e[1].record(stream)
 
+    def ev_pair():
+        return (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+
+    # warm-up steps, every call timed: per-call durations and the dominant call
     print(f"[bench] warmup {args.warmup} steps", file=sys.stderr, flush=True)
+    wev = [{c: ev_pair() for c in calls} for _ in range(args.warmup)]
     for i in range(args.warmup):
-        step(i)
+        step(i, wev[i])
     torch.cuda.synchronize()
+    skip = 1 if args.warmup > 1 else 0   # the first step also pays one-time costs
+    per_call_ms = {c: float(np.mean([e[c][0].elapsed_time(e[c][1]) for e in wev[skip:]]))
+                   for c in calls} if args.warmup else {c: float("nan") for c in calls}
+    single = ["forward", "backward", "update"]
+    dom = max(single, key=lambda c: per_call_ms[c]) if args.warmup else "backward"
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    # timed steps: start/stop around the whole region, one event pair around
+    # the dominant call of each step (on the stream its kernels run on)
+    tev = [{dom: ev_pair()} for _ in range(args.steps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     start.record(stream)
     for i in range(args.steps):
-        step(args.warmup + i, evs[i])
+        step(args.warmup + i, tev[i])
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_total = start.elapsed_time(stop)
     ms_step = ms_total / args.steps
-    calls = ["forward", "cast", "backward", "update"]
-    per_call_ms = {c: float(np.mean([e[k].elapsed_time(e[k + 1]) for e in evs]))
-                   for k, c in enumerate(calls)}
+    dom_ms = float(np.mean([e[dom][0].elapsed_time(e[dom][1]) for e in tev]))
     print(f"[bench] timed {args.steps} steps: {ms_step:.4f} ms/step (wall {wall:.3f} s)",
           file=sys.stderr, flush=True)
 
@@ -265,11 +277,9 @@ def main():
             nbytes[c] += v / args.steps
     step_bytes = sum(nbytes.values())
 
-    single = ["forward", "backward", "update"]
-    dom = max(single, key=lambda c: per_call_ms[c])
-    achieved = nbytes[dom] / (per_call_ms[dom] * 1e-3) / 1e9
+    achieved = nbytes[dom] / (dom_ms * 1e-3) / 1e9
     traffic = load_traffic(dom, args.config)
-    traffic_gbs = None if traffic is None else traffic / (per_call_ms[dom] * 1e-3) / 1e9
+    traffic_gbs = None if traffic is None else traffic / (dom_ms * 1e-3) / 1e9
     result = {
         "metric": "embedding train steps/sec (fwd+cast+bwd+update) and achieved HBM GB/s",
         "value": round(args.steps / (ms_total * 1e-3), 3),
@@ -293,10 +303,12 @@ def main():
         "step_algorithmic_frac_of_hbm_peak": round(step_bytes / (ms_step * 1e-3) / 1e9
                                                    / HBM_PEAK_GBS, 4),
         "per_call_us": {c: round(v * 1e3, 2) for c, v in per_call_ms.items()},
+        "per_call_us_measured_on": f"warm-up steps {skip}..{args.warmup - 1}, every call timed",
         "per_call_algorithmic_GBps": {c: round(nbytes[c] / (per_call_ms[c] * 1e-3) / 1e9, 1)
                                       for c in calls},
         "roofline": {"bound": "hbm", "call": f"tc_embed_{dom}" if dom != "update"
                      else "tc_sparse_update", "kernels": KERNEL_NAMES[dom],
+                     "launch_us": round(dom_ms * 1e3, 2),
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic,
