@@ -31,9 +31,9 @@ namespace {
 constexpr int kRadixBits = 8;
 constexpr int kRadix = 1 << kRadixBits;
 constexpr int kSortWaves = kBlock / kWave;        // 4
-constexpr int kItems = 16;                        // positions per lane per tile
-constexpr int kWaveSpan = kWave * kItems;         // 1024
-constexpr int kTile = kSortWaves * kWaveSpan;     // 4096
+constexpr int kItems = 8;                         // positions per lane per tile
+constexpr int kWaveSpan = kWave * kItems;         // 512
+constexpr int kTile = kSortWaves * kWaveSpan;     // 2048
 static_assert(kRadix == kBlock, "one thread per digit in the per-digit loops");
 
 __device__ __forceinline__ uint64_t lanemask_lt(int lane) { return (uint64_t(1) << lane) - 1; }
@@ -59,21 +59,46 @@ __global__ __launch_bounds__(kBlock) void k_build_keys(
 }
 
 // ---------------------------------------------------------------------------
-// 2a. per-tile digit histogram -> counts[digit * num_tiles + tile]
+// Lanes of a wavefront whose digit equals this lane's (BITS ballots), among
+// the lanes where ok holds.
+template <int BITS>
+__device__ __forceinline__ uint64_t match_digit(uint32_t d, bool ok) {
+    uint64_t peers = __ballot(ok);
+#pragma unroll
+    for (int b = 0; b < BITS; ++b) {
+        const bool bit = (d >> b) & 1u;
+        const uint64_t m = __ballot(bit);
+        peers &= bit ? m : ~m;
+    }
+    return peers;
+}
+
+// 2a. per-tile digit histogram -> counts[digit * num_tiles + tile]. Equal
+// digits within a wavefront are counted by one lane (no LDS atomic
+// conflicts under skewed keys).
+template <int BITS>
 __global__ __launch_bounds__(kBlock) void k_radix_hist(const int32_t *__restrict__ keys,
-                                                       int64_t n, int shift, int bits,
+                                                       int64_t n, int shift,
                                                        int32_t *__restrict__ counts,
                                                        int32_t num_tiles) {
     __shared__ int32_t hist[kSortWaves][kRadix];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
-    for (int i = tid; i < kSortWaves * kRadix; i += kBlock) (&hist[0][0])[i] = 0;
-    __syncthreads();
-    const uint32_t mask = (1u << bits) - 1u;
+    constexpr uint32_t mask = (1u << BITS) - 1u;
     const int64_t base = int64_t(blockIdx.x) * kTile + int64_t(w) * kWaveSpan;
-#pragma unroll 4
+    int32_t key[kItems];
+#pragma unroll
     for (int i = 0; i < kItems; ++i) {
         const int64_t j = base + i * kWave + lane;
-        if (j < n) atomicAdd(&hist[w][(uint32_t(keys[j]) >> shift) & mask], 1);
+        key[i] = j < n ? keys[j] : 0;
+    }
+    for (int i = tid; i < kSortWaves * kRadix; i += kBlock) (&hist[0][0])[i] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+        const bool ok = base + i * kWave + lane < n;
+        const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
+        const uint64_t peers = match_digit<BITS>(d, ok);
+        if (ok && (peers & lanemask_lt(lane)) == 0) atomicAdd(&hist[w][d], __popcll(peers));
     }
     __syncthreads();
     const int d = tid;
@@ -137,31 +162,27 @@ __global__ __launch_bounds__(kBlock) void k_radix_scan(int32_t *__restrict__ cou
 }
 
 // 2c. stable scatter of one tile. Ranks are computed as described at the
-// top; the tile is then laid out in sorted order in LDS and written back
-// thread by thread in that order, so neighbouring threads write
-// neighbouring addresses of the same digit run (coalesced stores instead of
-// one scattered store per pair).
+// top: within a wavefront the lanes holding equal digits are found with
+// ballots, the lowest of them adds their number to the wave's running count
+// of that digit with one LDS atomic (the returned old value is the count of
+// that digit in earlier items, since a wave's LDS operations complete in
+// order) and the others take it from that lane. The tile is then laid out in
+// sorted order in LDS and written back thread by thread in that order, so
+// neighbouring threads write neighbouring addresses of the same digit run
+// (coalesced stores instead of one scattered store per pair).
+template <int BITS>
 __global__ __launch_bounds__(kBlock) void k_radix_scatter(
     const int32_t *__restrict__ keys_in, const int32_t *__restrict__ vals_in,
     int32_t *__restrict__ keys_out, int32_t *__restrict__ vals_out, int64_t n, int shift,
-    int bits, const int32_t *__restrict__ counts, const int32_t *__restrict__ totals,
+    const int32_t *__restrict__ counts, const int32_t *__restrict__ totals,
     int32_t num_tiles) {
     __shared__ int32_t wcount[kSortWaves][kRadix];  // running, then exclusive over waves
-    __shared__ int32_t local_start[kRadix];          // first tile-local position per digit
+    __shared__ int32_t run_start[kSortWaves][kRadix];  // local start of wave w's digit d
     __shared__ int32_t run_shift[kRadix];            // global position - local position
     __shared__ int32_t stage_key[kTile];
     __shared__ int32_t stage_val[kTile];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
-    const uint32_t mask = (1u << bits) - 1u;
-
-    for (int i = tid; i < kSortWaves * kRadix; i += kBlock) (&wcount[0][0])[i] = 0;
-    int32_t tile_base;  // global start of this tile's run of digit `tid`
-    {
-        int32_t tot;
-        const int32_t digit_base = block_exclusive_scan(totals[tid], &tot);
-        tile_base = digit_base + counts[int64_t(tid) * num_tiles + blockIdx.x];
-    }
-    __syncthreads();
+    constexpr uint32_t mask = (1u << BITS) - 1u;
 
     const int64_t base = int64_t(blockIdx.x) * kTile + int64_t(w) * kWaveSpan;
     int32_t key[kItems], val[kItems], rank[kItems];
@@ -172,34 +193,49 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
         key[i] = ok ? keys_in[j] : 0;
         val[i] = ok ? vals_in[j] : 0;
     }
+    const int32_t total_d = totals[tid];
+    const int32_t count_d = counts[int64_t(tid) * num_tiles + blockIdx.x];
+    for (int i = tid; i < kSortWaves * kRadix; i += kBlock) (&wcount[0][0])[i] = 0;
+    int32_t tile_base;  // global start of this tile's run of digit `tid`
+    {
+        int32_t tot;
+        tile_base = block_exclusive_scan(total_d, &tot) + count_d;
+    }
+    __syncthreads();
+
+    // all atomics first, then the broadcasts, so no item waits for the LDS
+    // round trip of the one before it
+    int32_t lower_n[kItems], leader[kItems], old[kItems];
 #pragma unroll
     for (int i = 0; i < kItems; ++i) {
         const bool ok = base + i * kWave + lane < n;
         const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
-        uint64_t peers = __ballot(ok);
-        for (int b = 0; b < bits; ++b) {
-            const bool bit = (d >> b) & 1u;
-            const uint64_t m = __ballot(bit);
-            peers &= bit ? m : ~m;
-        }
+        const uint64_t peers = match_digit<BITS>(d, ok);
         const uint64_t lower = peers & lanemask_lt(lane);
-        const int32_t before = wcount[w][d];
-        rank[i] = before + __popcll(lower);
-        if (ok && lower == 0) wcount[w][d] = before + __popcll(peers);
+        lower_n[i] = __popcll(lower);
+        leader[i] = peers ? __builtin_ctzll(peers) : lane;
+        old[i] = 0;
+        if (ok && lower == 0) old[i] = atomicAdd(&wcount[w][d], __popcll(peers));
     }
+    // the leader (lowest peer) holds the count of the digit before this item
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) rank[i] = __shfl(old[i], leader[i], kWave) + lower_n[i];
     __syncthreads();
     {
         // per digit: exclusive prefix over waves, then over digits
-        int32_t s = 0;
+        int32_t s = 0, c[kSortWaves];
 #pragma unroll
-        for (int ww = 0; ww < kSortWaves; ++ww) {
-            const int32_t c = wcount[ww][tid];
-            wcount[ww][tid] = s;
-            s += c;
-        }
+        for (int ww = 0; ww < kSortWaves; ++ww) c[ww] = wcount[ww][tid];
+#pragma unroll
+        for (int ww = 0; ww < kSortWaves; ++ww) s += c[ww];
         int32_t tot;
         const int32_t start = block_exclusive_scan(s, &tot);
-        local_start[tid] = start;
+        int32_t r = start;
+#pragma unroll
+        for (int ww = 0; ww < kSortWaves; ++ww) {
+            run_start[ww][tid] = r;
+            r += c[ww];
+        }
         run_shift[tid] = tile_base - start;
     }
     __syncthreads();
@@ -208,7 +244,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
         const int64_t j = base + i * kWave + lane;
         if (j < n) {
             const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
-            const int32_t lp = local_start[d] + wcount[w][d] + rank[i];
+            const int32_t lp = run_start[w][d] + rank[i];
             stage_key[lp] = key[i];
             stage_val[lp] = val[i];
         }
@@ -328,6 +364,37 @@ __global__ void k_cast_empty(int32_t *seg_offsets, int32_t *num_unique) {
     }
 }
 
+// One LSD pass over `bits` (1..kRadixBits) digit bits starting at `shift`.
+tc_status launch_radix_pass(int bits, const int32_t *kin, const int32_t *vin, int32_t *kout,
+                            int32_t *vout, int64_t n, int shift, int32_t *counts,
+                            int32_t *totals, int32_t tiles, hipStream_t stream) {
+#define TC_PASS_CASE(B)                                                                      \
+    case B:                                                                                  \
+        k_radix_hist<B><<<tiles, kBlock, 0, stream>>>(kin, n, shift, counts, tiles);         \
+        if (check_launch("k_radix_hist") != TC_OK) return TC_ERR_HIP;                        \
+        k_radix_scan<<<kRadix, kBlock, 0, stream>>>(counts, tiles, totals);                  \
+        if (check_launch("k_radix_scan") != TC_OK) return TC_ERR_HIP;                        \
+        k_radix_scatter<B><<<tiles, kBlock, 0, stream>>>(kin, vin, kout, vout, n, shift,     \
+                                                         counts, totals, tiles);             \
+        return check_launch("k_radix_scatter");
+    switch (bits) {
+        TC_PASS_CASE(1)
+        TC_PASS_CASE(2)
+        TC_PASS_CASE(3)
+        TC_PASS_CASE(4)
+        TC_PASS_CASE(5)
+        TC_PASS_CASE(6)
+        TC_PASS_CASE(7)
+        TC_PASS_CASE(8)
+        default:
+            break;
+    }
+#undef TC_PASS_CASE
+    set_error("no radix pass for %d bits", bits);
+    return TC_ERR_UNSUPPORTED;
+}
+static_assert(kRadixBits == 8, "launch_radix_pass instantiates 1..8 bits");
+
 constexpr size_t kAlign = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -427,15 +494,8 @@ extern "C" tc_status tc_cast_index(const int64_t *table_row_offset, int32_t num_
         const int pb = (shift + per_pass <= bits) ? per_pass : bits - shift;
         const bool last = p == passes - 1;
         int32_t *vdst = last ? casted_src : vout;
-        k_radix_hist<<<tiles, kBlock, 0, stream>>>(kin, num_pairs, shift, pb, counts, tiles);
-        tc_status st = check_launch("k_radix_hist");
-        if (st != TC_OK) return st;
-        k_radix_scan<<<kRadix, kBlock, 0, stream>>>(counts, tiles, totals);
-        st = check_launch("k_radix_scan");
-        if (st != TC_OK) return st;
-        k_radix_scatter<<<tiles, kBlock, 0, stream>>>(kin, vin, kout, vdst, num_pairs, shift, pb,
-                                                      counts, totals, tiles);
-        st = check_launch("k_radix_scatter");
+        tc_status st = launch_radix_pass(pb, kin, vin, kout, vdst, num_pairs, shift, counts,
+                                         totals, tiles, stream);
         if (st != TC_OK) return st;
         // next pass reads what this one wrote
         int32_t *tk = kin, *tv = vin;
