@@ -204,7 +204,8 @@ def main():
     dev = torch.device("cuda", 0)
     trainer = tc.EmbeddingTrainer(total_rows=w.total_rows, dim=w.dim, num_tables=w.num_tables,
                                   bags_per_table=w.batch, max_pairs=max_pairs,
-                                  optimizer=w.optimizer, lr=w.lr, eps=w.eps, device=dev)
+                                  optimizer=w.optimizer, lr=w.lr, eps=w.eps, device=dev,
+                                  max_table_rows=w.rows_per_table)
     device_fill.fill_uniform(trainer.W, seed=0, lo=w.init_lo, hi=w.init_hi)
     dbat = [dict(off=torch.from_numpy(b.table_row_offset).to(dev),
                  idx=torch.from_numpy(b.indices).to(dev),

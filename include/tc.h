@@ -62,7 +62,7 @@
 extern "C" {
 #endif
 
-#define TC_ABI_VERSION 1
+#define TC_ABI_VERSION 2
 
 typedef enum tc_status {
     TC_OK = 0,
@@ -93,9 +93,10 @@ tc_status tc_embed_forward(const float *W, int64_t total_rows, int32_t dim,
 
 /*
  * Workspace bytes tc_cast_index needs for `num_pairs` pairs over
- * `total_rows` global rows (host function; launches nothing).
+ * `total_rows` global rows in `num_tables` tables (host function; launches
+ * nothing).
  */
-size_t tc_cast_workspace_bytes(int64_t num_pairs, int64_t total_rows);
+size_t tc_cast_workspace_bytes(int64_t num_pairs, int64_t total_rows, int32_t num_tables);
 
 /*
  * Tensor Casting (Algorithm 2). The (src, dst) pairs are sorted by src with
@@ -111,10 +112,18 @@ size_t tc_cast_workspace_bytes(int64_t num_pairs, int64_t total_rows);
  * holds min(num_pairs, total_rows) and seg_offsets one more. casted_dst may
  * be NULL (the backward pass does not need it). All outputs are int32 and
  * exact. `workspace` is device memory of at least
- * tc_cast_workspace_bytes(num_pairs, total_rows) bytes, 256-byte aligned.
+ * tc_cast_workspace_bytes(num_pairs, total_rows, num_tables) bytes, 256-byte
+ * aligned.
+ * max_table_rows (host) is an upper bound on the rows of every table, hence
+ * on every index, or 0 if unknown. It only selects the sort: with a bound
+ * much smaller than total_rows (and at most 256 tables) each table is sorted
+ * on its table-local row, which takes fewer radix passes; the results are
+ * the same either way. An index at or above a non-zero bound gives undefined
+ * results, as any out-of-range index does.
  */
 tc_status tc_cast_index(const int64_t *table_row_offset, int32_t num_tables,
-                        int32_t bags_per_table, int64_t total_rows, const int32_t *indices,
+                        int32_t bags_per_table, int64_t total_rows, int64_t max_table_rows,
+                        const int32_t *indices,
                         const int32_t *bag_offsets, int64_t num_pairs, int32_t *unique_rows,
                         int32_t *seg_offsets, int32_t *casted_src, int32_t *casted_dst,
                         int32_t *num_unique, void *workspace, size_t workspace_bytes,

@@ -1,16 +1,17 @@
 // Tensor Casting (Algorithm 2) on CDNA4.
 //
 //  1. k_build_keys   -- (src, dst) pairs from the bag-major CSR index:
-//                       key = global row, value = bag id.
-//  2. LSD radix sort by key, stable, kRadixBits bits per pass over the
-//     ceil(log2(total_rows)) bits that can be set. Each pass is
+//                       key = row, value = bag id. Block 0 also lays out the
+//                       sort segments (below).
+//  2. LSD radix sort by key, stable, at most kMaxRadixBits bits per pass over
+//     the key bits that can be set. Each pass is
 //       k_radix_hist    per-tile digit counts (LDS histograms, one per wave)
 //       k_radix_scan    per-digit exclusive scan over tiles (one block/digit)
-//       k_radix_scatter stable scatter: a wave ranks equal digits among its
-//                       64 lanes with kRadixBits ballots + popcount, keeps a
-//                       running per-digit count per wave in LDS, and waves
-//                       are combined in tile order; the tile is laid out in
-//                       sorted order in LDS and stored in that order.
+//       k_radix_scatter stable scatter: a wave finds the lanes holding equal
+//                       digits with ballots, counts them into its running
+//                       per-digit count in LDS, waves are combined in tile
+//                       order, and the tile is laid out in sorted order in
+//                       LDS and stored in that order.
 //     A pass reads and writes 8 bytes per pair plus a 4-byte read for the
 //     histogram. The last pass writes the values straight into casted_src.
 //  3. Segment build (the scan and cumulative sum of Algorithm 2):
@@ -18,95 +19,43 @@
 //       k_seg_scan   exclusive scan of tile head counts -> *num_unique
 //       k_seg_write  casted_dst, unique_rows, seg_offsets
 //
-// Tiles are kTile consecutive sorted positions; wave w of a block owns
-// positions [w*kWaveSpan, (w+1)*kWaveSpan) of its tile and walks them 64 at a
-// time, lane l taking position base + 64*i + l, so tile order = (wave,
-// iteration, lane) order and every pass is stable. No atomics on global
-// memory; nothing here depends on scheduling order.
+// Sort segments. The pairs of table t are contiguous in the input
+// (bag-major CSR, tables in order) and so are their rows in the output. When
+// the caller bounds the table sizes, each table is sorted on its
+// table-local row, which needs fewer key bits than the global row (32 tables
+// of 2^20 rows: 20 bits, three passes, instead of 25 bits and four), and the
+// last pass adds the table's row offset back. A segment is cut into tiles of
+// kTile pairs (its last tile may be short), tiles of all segments are
+// numbered in segment order, and a digit's position inside its segment comes
+// from the per-digit scan over all tiles minus that scan at the segment's
+// first tile. k_build_keys writes one record per tile (its pair range and its
+// segment's), so a pass kernel finds its tile with a single load. Without a
+// bound there is one segment, all pairs on global rows, and tiles are plain
+// slices of kTile pairs.
+//
+// Within a tile, wave w owns positions [w*kWaveSpan, (w+1)*kWaveSpan) and
+// walks them 64 at a time, lane l taking position base + 64*i + l, so tile
+// order = (wave, iteration, lane) order and every pass is stable. No atomics
+// on global memory; nothing here depends on scheduling order.
 #include "tc_internal.h"
 
 namespace tc {
 namespace {
 
-constexpr int kRadixBits = 8;
-constexpr int kRadix = 1 << kRadixBits;
+// Digits of at most 8 bits: with 2048-pair tiles, wider digits cost more
+// per-tile digit bookkeeping (counts written, scanned and read back for every
+// digit of every tile) than the pass they save, at these sizes.
+constexpr int kMaxRadixBits = 8;
+constexpr int kMaxRadix = 1 << kMaxRadixBits;
 constexpr int kSortWaves = kBlock / kWave;        // 4
 constexpr int kItems = 8;                         // positions per lane per tile
 constexpr int kWaveSpan = kWave * kItems;         // 512
 constexpr int kTile = kSortWaves * kWaveSpan;     // 2048
-static_assert(kRadix == kBlock, "one thread per digit in the per-digit loops");
+// Table-local sorting for at most this many tables (one thread per table
+// lays the segments out).
+constexpr int kMaxSegTables = kBlock;
 
 __device__ __forceinline__ uint64_t lanemask_lt(int lane) { return (uint64_t(1) << lane) - 1; }
-
-// ---------------------------------------------------------------------------
-// 1. key build: one group of 16 lanes per bag writes that bag's pairs.
-__global__ __launch_bounds__(kBlock) void k_build_keys(
-    const int32_t *__restrict__ indices, const int32_t *__restrict__ bag_offsets,
-    const int64_t *__restrict__ table_row_offset, int64_t num_bags, int32_t bags_per_table,
-    int32_t *__restrict__ keys, int32_t *__restrict__ vals) {
-    constexpr int kLanes = 16;
-    const int64_t group = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / kLanes;
-    const int64_t ngroups = (int64_t(gridDim.x) * blockDim.x) / kLanes;
-    const int sub = threadIdx.x & (kLanes - 1);
-    for (int64_t g = group; g < num_bags; g += ngroups) {
-        const int32_t beg = bag_offsets[g], end = bag_offsets[g + 1];
-        const int64_t base = table_row_offset[g / bags_per_table];
-        for (int32_t j = beg + sub; j < end; j += kLanes) {
-            keys[j] = int32_t(base + indices[j]);
-            vals[j] = int32_t(g);
-        }
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Lanes of a wavefront whose digit equals this lane's (BITS ballots), among
-// the lanes where ok holds.
-template <int BITS>
-__device__ __forceinline__ uint64_t match_digit(uint32_t d, bool ok) {
-    uint64_t peers = __ballot(ok);
-#pragma unroll
-    for (int b = 0; b < BITS; ++b) {
-        const bool bit = (d >> b) & 1u;
-        const uint64_t m = __ballot(bit);
-        peers &= bit ? m : ~m;
-    }
-    return peers;
-}
-
-// 2a. per-tile digit histogram -> counts[digit * num_tiles + tile]. Equal
-// digits within a wavefront are counted by one lane (no LDS atomic
-// conflicts under skewed keys).
-template <int BITS>
-__global__ __launch_bounds__(kBlock) void k_radix_hist(const int32_t *__restrict__ keys,
-                                                       int64_t n, int shift,
-                                                       int32_t *__restrict__ counts,
-                                                       int32_t num_tiles) {
-    __shared__ int32_t hist[kSortWaves][kRadix];
-    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
-    constexpr uint32_t mask = (1u << BITS) - 1u;
-    const int64_t base = int64_t(blockIdx.x) * kTile + int64_t(w) * kWaveSpan;
-    int32_t key[kItems];
-#pragma unroll
-    for (int i = 0; i < kItems; ++i) {
-        const int64_t j = base + i * kWave + lane;
-        key[i] = j < n ? keys[j] : 0;
-    }
-    for (int i = tid; i < kSortWaves * kRadix; i += kBlock) (&hist[0][0])[i] = 0;
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < kItems; ++i) {
-        const bool ok = base + i * kWave + lane < n;
-        const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
-        const uint64_t peers = match_digit<BITS>(d, ok);
-        if (ok && (peers & lanemask_lt(lane)) == 0) atomicAdd(&hist[w][d], __popcll(peers));
-    }
-    __syncthreads();
-    const int d = tid;
-    int32_t s = 0;
-#pragma unroll
-    for (int ww = 0; ww < kSortWaves; ++ww) s += hist[ww][d];
-    counts[int64_t(d) * num_tiles + blockIdx.x] = s;
-}
 
 // Block-wide exclusive scan of one value per thread; returns the prefix and
 // writes the block total to *total.
@@ -133,19 +82,161 @@ __device__ __forceinline__ int32_t block_exclusive_scan(int32_t v, int32_t *tota
     return wbase + incl - v;
 }
 
+// One tile of a radix pass: pairs [p0, p1) of segment s, whose tiles are
+// [first, next), whose pairs start at pstart, and whose keys get rowoff added
+// by the last pass. Tiles past the last one have p0 = p1 = 0 and s = -1.
+struct alignas(16) TileRec {
+    int32_t p0, p1, first, next, pstart, rowoff, s, pad;
+};
+// ---------------------------------------------------------------------------
+// 1. key build: one group of 16 lanes per bag writes that bag's pairs; keys
+// are table-local rows when `local`, else global rows. With `local`, block 0
+// also writes the tile records of the num_tables segments.
+__global__ __launch_bounds__(kBlock) void k_build_keys(
+    const int32_t *__restrict__ indices, const int32_t *__restrict__ bag_offsets,
+    const int64_t *__restrict__ table_row_offset, int64_t num_bags, int32_t bags_per_table,
+    int32_t num_tables, bool local, TileRec *__restrict__ tiles, int32_t num_tile_slots,
+    int32_t *__restrict__ keys, int32_t *__restrict__ vals) {
+    if (local && blockIdx.x == 0) {
+        __shared__ int32_t tstart[kMaxSegTables + 1], pstart[kMaxSegTables + 1];
+        __shared__ int32_t rowoff[kMaxSegTables];
+        const int t = threadIdx.x;
+        int32_t p0 = 0, n_t = 0;
+        if (t < num_tables) {
+            p0 = bag_offsets[int64_t(t) * bags_per_table];
+            n_t = bag_offsets[int64_t(t + 1) * bags_per_table] - p0;
+            rowoff[t] = int32_t(table_row_offset[t]);
+        }
+        int32_t total;
+        const int32_t ts = block_exclusive_scan((n_t + kTile - 1) / kTile, &total);
+        if (t < num_tables) {
+            tstart[t] = ts;
+            pstart[t] = p0;
+        }
+        if (t == 0) {
+            tstart[num_tables] = total;
+            pstart[num_tables] = bag_offsets[num_bags];
+        }
+        __syncthreads();
+        for (int32_t b = t; b < num_tile_slots; b += kBlock) {
+            TileRec r{0, 0, 0, 0, 0, 0, -1, 0};
+            if (b < total) {
+                // the segment holding tile b: last s with tstart[s] <= b
+                // (segments without pairs have no tiles and are passed over)
+                int32_t lo = 0, hi = num_tables - 1;
+                while (lo < hi) {
+                    const int32_t mid = (lo + hi + 1) / 2;
+                    if (tstart[mid] <= b) lo = mid; else hi = mid - 1;
+                }
+                const int32_t sg = lo;
+                r.s = sg;
+                r.first = tstart[sg];
+                r.next = tstart[sg + 1];
+                r.pstart = pstart[sg];
+                r.rowoff = rowoff[sg];
+                r.p0 = pstart[sg] + (b - r.first) * kTile;
+                const int32_t end = pstart[sg + 1];
+                r.p1 = r.p0 + kTile < end ? r.p0 + kTile : end;
+            }
+            tiles[b] = r;
+        }
+    }
+    constexpr int kLanes = 16;
+    const int64_t group = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / kLanes;
+    const int64_t ngroups = (int64_t(gridDim.x) * blockDim.x) / kLanes;
+    const int sub = threadIdx.x & (kLanes - 1);
+    for (int64_t g = group; g < num_bags; g += ngroups) {
+        const int32_t beg = bag_offsets[g], end = bag_offsets[g + 1];
+        const int64_t base = local ? 0 : table_row_offset[g / bags_per_table];
+        for (int32_t j = beg + sub; j < end; j += kLanes) {
+            keys[j] = int32_t(base + indices[j]);
+            vals[j] = int32_t(g);
+        }
+    }
+}
+
+// This block's tile: its record (table-local sort) or a plain slice of the
+// n pairs (global sort: one segment, tiles 0 .. ceil(n/kTile)-1).
+__device__ __forceinline__ TileRec tile_of(const TileRec *__restrict__ tiles, int32_t n) {
+    if (tiles) return tiles[blockIdx.x];
+    const int32_t used = (n + kTile - 1) / kTile;
+    const int32_t p0 = int32_t(blockIdx.x) * kTile;
+    TileRec r{0, 0, 0, used, 0, 0, -1, 0};
+    if (p0 < n) {
+        r.s = 0;
+        r.p0 = p0;
+        r.p1 = p0 + kTile < n ? p0 + kTile : n;
+    }
+    return r;
+}
+
+// Lanes of a wavefront whose digit equals this lane's (BITS ballots), among
+// the lanes where ok holds.
+template <int BITS>
+__device__ __forceinline__ uint64_t match_digit(uint32_t d, bool ok) {
+    uint64_t peers = __ballot(ok);
+#pragma unroll
+    for (int b = 0; b < BITS; ++b) {
+        const bool bit = (d >> b) & 1u;
+        const uint64_t m = __ballot(bit);
+        peers &= bit ? m : ~m;
+    }
+    return peers;
+}
+
+// ---------------------------------------------------------------------------
+// 2a. per-tile digit histogram -> counts[digit * tiles + tile]. Equal digits
+// within a wavefront are counted by one lane (no LDS atomic conflicts under
+// skewed keys). Blocks past the last tile write zeros.
+template <int BITS>
+__global__ __launch_bounds__(kBlock) void k_radix_hist(const int32_t *__restrict__ keys,
+                                                       int32_t n, int shift,
+                                                       const TileRec *__restrict__ recs,
+                                                       int32_t *__restrict__ counts,
+                                                       int32_t tiles) {
+    constexpr int R = 1 << BITS;
+    __shared__ int32_t hist[kSortWaves][R];
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+    constexpr uint32_t mask = R - 1u;
+    const TileRec tr = tile_of(recs, n);
+    const int32_t base = tr.p0 + w * kWaveSpan;
+    int32_t key[kItems];
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+        const int32_t j = base + i * kWave + lane;
+        key[i] = j < tr.p1 ? keys[j] : 0;
+    }
+    for (int i = tid; i < kSortWaves * R; i += kBlock) (&hist[0][0])[i] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+        const bool ok = base + i * kWave + lane < tr.p1;
+        const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
+        const uint64_t peers = match_digit<BITS>(d, ok);
+        if (ok && (peers & lanemask_lt(lane)) == 0) atomicAdd(&hist[w][d], __popcll(peers));
+    }
+    __syncthreads();
+    for (int d = tid; d < R; d += kBlock) {
+        int32_t s = 0;
+#pragma unroll
+        for (int ww = 0; ww < kSortWaves; ++ww) s += hist[ww][d];
+        counts[int64_t(d) * tiles + blockIdx.x] = s;
+    }
+}
+
 // 2b. counts[d][*] -> exclusive prefix over tiles (in place); totals[d].
 __global__ __launch_bounds__(kBlock) void k_radix_scan(int32_t *__restrict__ counts,
-                                                       int32_t num_tiles,
+                                                       int32_t tiles,
                                                        int32_t *__restrict__ totals) {
     constexpr int kPer = 4;
-    int32_t *row = counts + int64_t(blockIdx.x) * num_tiles;
+    int32_t *row = counts + int64_t(blockIdx.x) * tiles;
     int32_t carry = 0;
-    for (int32_t base = 0; base < num_tiles; base += kBlock * kPer) {
+    for (int32_t base = 0; base < tiles; base += kBlock * kPer) {
         int32_t v[kPer], s = 0;
 #pragma unroll
         for (int k = 0; k < kPer; ++k) {
             const int32_t i = base + threadIdx.x * kPer + k;
-            v[k] = i < num_tiles ? row[i] : 0;
+            v[k] = i < tiles ? row[i] : 0;
             s += v[k];
         }
         int32_t tot;
@@ -153,7 +244,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scan(int32_t *__restrict__ cou
 #pragma unroll
         for (int k = 0; k < kPer; ++k) {
             const int32_t i = base + threadIdx.x * kPer + k;
-            if (i < num_tiles) row[i] = p;
+            if (i < tiles) row[i] = p;
             p += v[k];
         }
         carry += tot;
@@ -161,45 +252,68 @@ __global__ __launch_bounds__(kBlock) void k_radix_scan(int32_t *__restrict__ cou
     if (threadIdx.x == 0) totals[blockIdx.x] = carry;
 }
 
-// 2c. stable scatter of one tile. Ranks are computed as described at the
-// top: within a wavefront the lanes holding equal digits are found with
-// ballots, the lowest of them adds their number to the wave's running count
-// of that digit with one LDS atomic (the returned old value is the count of
-// that digit in earlier items, since a wave's LDS operations complete in
-// order) and the others take it from that lane. The tile is then laid out in
-// sorted order in LDS and written back thread by thread in that order, so
-// neighbouring threads write neighbouring addresses of the same digit run
-// (coalesced stores instead of one scattered store per pair).
+// 2c. stable scatter of one tile. Within a wavefront the lanes holding equal
+// digits are found with ballots; the lowest of them adds their number to the
+// wave's running count of that digit with one LDS atomic (the returned old
+// value is the count of that digit in earlier items, since a wave's LDS
+// operations complete in order) and the others take it from that lane. The
+// tile is then laid out in sorted order in LDS and written back thread by
+// thread in that order, so neighbouring threads write neighbouring addresses
+// of the same digit run (coalesced stores instead of one scattered store per
+// pair). With add_rowoff the keys leave with the segment's row offset added.
 template <int BITS>
 __global__ __launch_bounds__(kBlock) void k_radix_scatter(
     const int32_t *__restrict__ keys_in, const int32_t *__restrict__ vals_in,
-    int32_t *__restrict__ keys_out, int32_t *__restrict__ vals_out, int64_t n, int shift,
-    const int32_t *__restrict__ counts, const int32_t *__restrict__ totals,
-    int32_t num_tiles) {
-    __shared__ int32_t wcount[kSortWaves][kRadix];  // running, then exclusive over waves
-    __shared__ int32_t run_start[kSortWaves][kRadix];  // local start of wave w's digit d
-    __shared__ int32_t run_shift[kRadix];            // global position - local position
+    int32_t *__restrict__ keys_out, int32_t *__restrict__ vals_out, int32_t n, int shift,
+    const TileRec *__restrict__ recs, const int32_t *__restrict__ counts,
+    const int32_t *__restrict__ totals, int32_t tiles, bool add_rowoff) {
+    constexpr int R = 1 << BITS;
+    constexpr int DPT = R > kBlock ? R / kBlock : 1;  // digits per thread
+    constexpr uint32_t mask = R - 1u;
+    // wave w's running count of digit d, then the tile-local start of its run
+    __shared__ int32_t wcount[kSortWaves][R];
+    __shared__ int32_t run_shift[R];  // global position - tile-local position
     __shared__ int32_t stage_key[kTile];
     __shared__ int32_t stage_val[kTile];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
-    constexpr uint32_t mask = (1u << BITS) - 1u;
+    const TileRec tr = tile_of(recs, n);
+    if (tr.s < 0) return;  // uniform: past the last tile
 
-    const int64_t base = int64_t(blockIdx.x) * kTile + int64_t(w) * kWaveSpan;
+    const int32_t base = tr.p0 + w * kWaveSpan;
     int32_t key[kItems], val[kItems], rank[kItems];
 #pragma unroll
     for (int i = 0; i < kItems; ++i) {
-        const int64_t j = base + i * kWave + lane;
-        const bool ok = j < n;
+        const int32_t j = base + i * kWave + lane;
+        const bool ok = j < tr.p1;
         key[i] = ok ? keys_in[j] : 0;
         val[i] = ok ? vals_in[j] : 0;
     }
-    const int32_t total_d = totals[tid];
-    const int32_t count_d = counts[int64_t(tid) * num_tiles + blockIdx.x];
-    for (int i = tid; i < kSortWaves * kRadix; i += kBlock) (&wcount[0][0])[i] = 0;
-    int32_t tile_base;  // global start of this tile's run of digit `tid`
+    // Thread tid handles digits tid*DPT .. tid*DPT+DPT-1 (digit order): where
+    // this tile's run of each digit starts in the output.
+    const int32_t first = tr.first, next = tr.next;
+    int32_t tile_off[DPT], seg_tot[DPT], my = 0;
+#pragma unroll
+    for (int k = 0; k < DPT; ++k) {
+        const int32_t d = tid * DPT + k;
+        tile_off[k] = seg_tot[k] = 0;
+        if (d < R) {
+            const int64_t row = int64_t(d) * tiles;
+            const int32_t at_first = counts[row + first];
+            tile_off[k] = counts[row + blockIdx.x] - at_first;
+            seg_tot[k] = (next < tiles ? counts[row + next] : totals[d]) - at_first;
+        }
+        my += seg_tot[k];
+    }
+    for (int i = tid; i < kSortWaves * R; i += kBlock) (&wcount[0][0])[i] = 0;
+    int32_t digit_base[DPT];
     {
         int32_t tot;
-        tile_base = block_exclusive_scan(total_d, &tot) + count_d;
+        int32_t p = block_exclusive_scan(my, &tot) + tr.pstart;
+#pragma unroll
+        for (int k = 0; k < DPT; ++k) {
+            digit_base[k] = p + tile_off[k];
+            p += seg_tot[k];
+        }
     }
     __syncthreads();
 
@@ -208,7 +322,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
     int32_t lower_n[kItems], leader[kItems], old[kItems];
 #pragma unroll
     for (int i = 0; i < kItems; ++i) {
-        const bool ok = base + i * kWave + lane < n;
+        const bool ok = base + i * kWave + lane < tr.p1;
         const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
         const uint64_t peers = match_digit<BITS>(d, ok);
         const uint64_t lower = peers & lanemask_lt(lane);
@@ -222,36 +336,48 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
     for (int i = 0; i < kItems; ++i) rank[i] = __shfl(old[i], leader[i], kWave) + lower_n[i];
     __syncthreads();
     {
-        // per digit: exclusive prefix over waves, then over digits
-        int32_t s = 0, c[kSortWaves];
+        // per digit: tile-local start of each wave's run (digit order, then
+        // wave order) and the shift from tile-local to global positions
+        int32_t c[DPT][kSortWaves], my_n = 0;
 #pragma unroll
-        for (int ww = 0; ww < kSortWaves; ++ww) c[ww] = wcount[ww][tid];
+        for (int k = 0; k < DPT; ++k) {
+            const int32_t d = tid * DPT + k;
 #pragma unroll
-        for (int ww = 0; ww < kSortWaves; ++ww) s += c[ww];
-        int32_t tot;
-        const int32_t start = block_exclusive_scan(s, &tot);
-        int32_t r = start;
-#pragma unroll
-        for (int ww = 0; ww < kSortWaves; ++ww) {
-            run_start[ww][tid] = r;
-            r += c[ww];
+            for (int ww = 0; ww < kSortWaves; ++ww) {
+                c[k][ww] = d < R ? wcount[ww][d] : 0;
+                my_n += c[k][ww];
+            }
         }
-        run_shift[tid] = tile_base - start;
+        int32_t tot;
+        int32_t start = block_exclusive_scan(my_n, &tot);
+#pragma unroll
+        for (int k = 0; k < DPT; ++k) {
+            const int32_t d = tid * DPT + k;
+            if (d < R) {
+                run_shift[d] = digit_base[k] - start;
+                int32_t r = start;
+#pragma unroll
+                for (int ww = 0; ww < kSortWaves; ++ww) {
+                    wcount[ww][d] = r;
+                    r += c[k][ww];
+                }
+                start = r;
+            }
+        }
     }
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < kItems; ++i) {
-        const int64_t j = base + i * kWave + lane;
-        if (j < n) {
+        if (base + i * kWave + lane < tr.p1) {
             const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
-            const int32_t lp = run_start[w][d] + rank[i];
+            const int32_t lp = wcount[w][d] + rank[i];
             stage_key[lp] = key[i];
             stage_val[lp] = val[i];
         }
     }
     __syncthreads();
-    const int64_t tile0 = int64_t(blockIdx.x) * kTile;
-    const int32_t in_tile = int32_t(n - tile0 < kTile ? n - tile0 : kTile);
+    const int32_t in_tile = tr.p1 - tr.p0;
+    const int32_t koff = add_rowoff ? tr.rowoff : 0;
 #pragma unroll
     for (int i = 0; i < kItems; ++i) {
         const int32_t lp = i * kBlock + tid;
@@ -259,7 +385,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
             const int32_t k = stage_key[lp];
             const uint32_t d = (uint32_t(k) >> shift) & mask;
             const int32_t pos = run_shift[d] + lp;
-            keys_out[pos] = k;
+            keys_out[pos] = k + koff;
             vals_out[pos] = stage_val[lp];
         }
     }
@@ -364,18 +490,19 @@ __global__ void k_cast_empty(int32_t *seg_offsets, int32_t *num_unique) {
     }
 }
 
-// One LSD pass over `bits` (1..kRadixBits) digit bits starting at `shift`.
+// One LSD pass over `bits` (1..kMaxRadixBits) digit bits starting at `shift`.
 tc_status launch_radix_pass(int bits, const int32_t *kin, const int32_t *vin, int32_t *kout,
-                            int32_t *vout, int64_t n, int shift, int32_t *counts,
-                            int32_t *totals, int32_t tiles, hipStream_t stream) {
+                            int32_t *vout, int32_t n, int shift, const TileRec *recs,
+                            int32_t *counts, int32_t *totals, int32_t tiles, bool last,
+                            hipStream_t stream) {
 #define TC_PASS_CASE(B)                                                                      \
     case B:                                                                                  \
-        k_radix_hist<B><<<tiles, kBlock, 0, stream>>>(kin, n, shift, counts, tiles);         \
+        k_radix_hist<B><<<tiles, kBlock, 0, stream>>>(kin, n, shift, recs, counts, tiles);   \
         if (check_launch("k_radix_hist") != TC_OK) return TC_ERR_HIP;                        \
-        k_radix_scan<<<kRadix, kBlock, 0, stream>>>(counts, tiles, totals);                  \
+        k_radix_scan<<<1 << B, kBlock, 0, stream>>>(counts, tiles, totals);                  \
         if (check_launch("k_radix_scan") != TC_OK) return TC_ERR_HIP;                        \
         k_radix_scatter<B><<<tiles, kBlock, 0, stream>>>(kin, vin, kout, vout, n, shift,     \
-                                                         counts, totals, tiles);             \
+                                                         recs, counts, totals, tiles, last); \
         return check_launch("k_radix_scatter");
     switch (bits) {
         TC_PASS_CASE(1)
@@ -393,35 +520,45 @@ tc_status launch_radix_pass(int bits, const int32_t *kin, const int32_t *vin, in
     set_error("no radix pass for %d bits", bits);
     return TC_ERR_UNSUPPORTED;
 }
-static_assert(kRadixBits == 8, "launch_radix_pass instantiates 1..8 bits");
+static_assert(kMaxRadixBits == 8, "launch_radix_pass instantiates 1..8 bits");
 
 constexpr size_t kAlign = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+// Sort segments available to a call with num_tables tables.
+inline int32_t seg_capacity(int32_t num_tables) {
+    return num_tables >= 1 && num_tables <= kMaxSegTables ? num_tables : 1;
+}
+
 struct CastPlan {
-    int64_t num_tiles;
-    size_t off_ka, off_va, off_kb, off_vb, off_counts, off_totals, off_heads, bytes;
+    int64_t sort_tiles;  // tile slots of a radix pass (all segments)
+    int64_t seg_tiles;   // tiles of the segment build (plain tiles of kTile)
+    size_t off_ka, off_va, off_kb, off_vb, off_counts, off_totals, off_heads, off_recs, bytes;
 };
 
-inline CastPlan cast_plan(int64_t n) {
+inline CastPlan cast_plan(int64_t n, int32_t num_tables) {
     CastPlan p{};
-    p.num_tiles = (n + kTile - 1) / kTile;
+    const int32_t nseg = seg_capacity(num_tables);
+    p.seg_tiles = (n + kTile - 1) / kTile;
+    p.sort_tiles = p.seg_tiles + nseg;  // each segment adds at most one short tile
     const size_t arr = align_up(size_t(n) * 4);
     size_t o = 0;
     p.off_ka = o; o += arr;
     p.off_va = o; o += arr;
     p.off_kb = o; o += arr;
     p.off_vb = o; o += arr;
-    p.off_counts = o; o += align_up(size_t(kRadix) * size_t(p.num_tiles) * 4);
-    p.off_totals = o; o += align_up(size_t(kRadix) * 4);
-    p.off_heads = o; o += align_up(size_t(p.num_tiles) * 4);
+    p.off_counts = o; o += align_up(size_t(kMaxRadix) * size_t(p.sort_tiles) * 4);
+    p.off_totals = o; o += align_up(size_t(kMaxRadix) * 4);
+    p.off_heads = o; o += align_up(size_t(p.seg_tiles) * 4);
+    p.off_recs = o; o += align_up(size_t(p.sort_tiles) * sizeof(TileRec));
     p.bytes = o;
     return p;
 }
 
-inline int key_bits(int64_t total_rows) {
+// bits needed for keys in [0, rows)
+inline int key_bits(int64_t rows) {
     int b = 0;
-    while (b < 31 && (int64_t(1) << b) < total_rows) ++b;
+    while (b < 31 && (int64_t(1) << b) < rows) ++b;
     return b < 1 ? 1 : b;  // at least one pass, so the values are always moved
 }
 
@@ -430,20 +567,23 @@ inline int key_bits(int64_t total_rows) {
 
 using namespace tc;
 
-extern "C" size_t tc_cast_workspace_bytes(int64_t num_pairs, int64_t total_rows) {
+extern "C" size_t tc_cast_workspace_bytes(int64_t num_pairs, int64_t total_rows,
+                                          int32_t num_tables) {
     (void)total_rows;
     if (num_pairs < 0) return 0;
-    return cast_plan(num_pairs).bytes;
+    return cast_plan(num_pairs, num_tables).bytes;
 }
 
 extern "C" tc_status tc_cast_index(const int64_t *table_row_offset, int32_t num_tables,
                                    int32_t bags_per_table, int64_t total_rows,
-                                   const int32_t *indices, const int32_t *bag_offsets,
-                                   int64_t num_pairs, int32_t *unique_rows, int32_t *seg_offsets,
+                                   int64_t max_table_rows, const int32_t *indices,
+                                   const int32_t *bag_offsets, int64_t num_pairs,
+                                   int32_t *unique_rows, int32_t *seg_offsets,
                                    int32_t *casted_src, int32_t *casted_dst, int32_t *num_unique,
                                    void *workspace, size_t workspace_bytes, hipStream_t stream) {
     clear_error();
-    TC_REQUIRE(num_tables >= 0 && bags_per_table >= 0 && total_rows >= 0 && num_pairs >= 0,
+    TC_REQUIRE(num_tables >= 0 && bags_per_table >= 0 && total_rows >= 0 && num_pairs >= 0 &&
+                   max_table_rows >= 0,
                TC_ERR_INVALID_ARG, "tc_cast_index: negative size");
     TC_REQUIRE(total_rows < (int64_t(1) << 31) && num_pairs < (int64_t(1) << 31),
                TC_ERR_INVALID_ARG, "tc_cast_index: total_rows and num_pairs must be below 2^31");
@@ -459,13 +599,20 @@ extern "C" tc_status tc_cast_index(const int64_t *table_row_offset, int32_t num_
                "tc_cast_index: pairs without bags or rows");
     TC_REQUIRE(table_row_offset && indices && bag_offsets && unique_rows && casted_src,
                TC_ERR_INVALID_ARG, "tc_cast_index: null pointer");
-    const CastPlan plan = cast_plan(num_pairs);
+    const CastPlan plan = cast_plan(num_pairs, num_tables);
     TC_REQUIRE(workspace && workspace_bytes >= plan.bytes, TC_ERR_WORKSPACE,
                "tc_cast_index: workspace of %zu bytes, %zu needed", workspace_bytes, plan.bytes);
     TC_REQUIRE((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) == 0, TC_ERR_WORKSPACE,
                "tc_cast_index: workspace must be 256-byte aligned");
-    TC_REQUIRE(plan.num_tiles < (int64_t(1) << 31) / kRadix, TC_ERR_INVALID_ARG,
+    TC_REQUIRE(plan.sort_tiles < (int64_t(1) << 31) / kMaxRadix, TC_ERR_INVALID_ARG,
                "tc_cast_index: too many pairs");
+
+    // Table-local keys when the tables are known to be small enough to save
+    // key bits; otherwise one segment of global rows.
+    const int global_bits = key_bits(total_rows);
+    const bool local = max_table_rows > 0 && num_tables <= kMaxSegTables &&
+                       key_bits(max_table_rows) < global_bits;
+    const int bits = local ? key_bits(max_table_rows) : global_bits;
 
     char *ws = static_cast<char *>(workspace);
     int32_t *ka = reinterpret_cast<int32_t *>(ws + plan.off_ka);
@@ -475,18 +622,20 @@ extern "C" tc_status tc_cast_index(const int64_t *table_row_offset, int32_t num_
     int32_t *counts = reinterpret_cast<int32_t *>(ws + plan.off_counts);
     int32_t *totals = reinterpret_cast<int32_t *>(ws + plan.off_totals);
     int32_t *heads = reinterpret_cast<int32_t *>(ws + plan.off_heads);
-    const int32_t tiles = int32_t(plan.num_tiles);
+    TileRec *recs = local ? reinterpret_cast<TileRec *>(ws + plan.off_recs) : nullptr;
+    const int32_t sort_tiles = int32_t(plan.sort_tiles);
+    const int32_t seg_tiles = int32_t(plan.seg_tiles);
 
     {
         const unsigned grid = grid_for(num_bags, kBlock / 16, int64_t(kNumCUs) * 8);
         k_build_keys<<<grid, kBlock, 0, stream>>>(indices, bag_offsets, table_row_offset,
-                                                  num_bags, bags_per_table, ka, va);
+                                                  num_bags, bags_per_table, num_tables, local,
+                                                  recs, sort_tiles, ka, va);
         tc_status st = check_launch("k_build_keys");
         if (st != TC_OK) return st;
     }
 
-    const int bits = key_bits(total_rows);
-    const int passes = (bits + kRadixBits - 1) / kRadixBits;
+    const int passes = (bits + kMaxRadixBits - 1) / kMaxRadixBits;
     const int per_pass = (bits + passes - 1) / passes;
     int32_t *kin = ka, *vin = va, *kout = kb, *vout = vb;
     for (int p = 0; p < passes; ++p) {
@@ -494,8 +643,8 @@ extern "C" tc_status tc_cast_index(const int64_t *table_row_offset, int32_t num_
         const int pb = (shift + per_pass <= bits) ? per_pass : bits - shift;
         const bool last = p == passes - 1;
         int32_t *vdst = last ? casted_src : vout;
-        tc_status st = launch_radix_pass(pb, kin, vin, kout, vdst, num_pairs, shift, counts,
-                                         totals, tiles, stream);
+        tc_status st = launch_radix_pass(pb, kin, vin, kout, vdst, int32_t(num_pairs), shift,
+                                         recs, counts, totals, sort_tiles, last, stream);
         if (st != TC_OK) return st;
         // next pass reads what this one wrote
         int32_t *tk = kin, *tv = vin;
@@ -506,13 +655,13 @@ extern "C" tc_status tc_cast_index(const int64_t *table_row_offset, int32_t num_
     }
     const int32_t *sorted_keys = kin;
 
-    k_seg_count<<<tiles, kBlock, 0, stream>>>(sorted_keys, num_pairs, heads);
+    k_seg_count<<<seg_tiles, kBlock, 0, stream>>>(sorted_keys, num_pairs, heads);
     tc_status st = check_launch("k_seg_count");
     if (st != TC_OK) return st;
-    k_seg_scan<<<1, kBlock, 0, stream>>>(heads, tiles, num_unique);
+    k_seg_scan<<<1, kBlock, 0, stream>>>(heads, seg_tiles, num_unique);
     st = check_launch("k_seg_scan");
     if (st != TC_OK) return st;
-    k_seg_write<<<tiles, kBlock, 0, stream>>>(sorted_keys, num_pairs, heads, unique_rows,
-                                              seg_offsets, casted_dst);
+    k_seg_write<<<seg_tiles, kBlock, 0, stream>>>(sorted_keys, num_pairs, heads, unique_rows,
+                                                  seg_offsets, casted_dst);
     return check_launch("k_seg_write");
 }

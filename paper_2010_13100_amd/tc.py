@@ -23,9 +23,9 @@ _vp, _i32, _i64, _f32, _sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, c
 
 _SIGNATURES = {
     "tc_embed_forward": (_i32, [_vp, _i64, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _vp]),
-    "tc_cast_workspace_bytes": (_sz, [_i64, _i64]),
-    "tc_cast_index": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp,
-                             _vp, _sz, _vp]),
+    "tc_cast_workspace_bytes": (_sz, [_i64, _i64, _i32]),
+    "tc_cast_index": (_i32, [_vp, _i32, _i32, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp,
+                             _vp, _vp, _sz, _vp]),
     "tc_embed_backward": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _i64, _vp, _vp]),
     "tc_sparse_update": (_i32, [_vp, _vp, _i64, _i32, _vp, _vp, _vp, _i64, _i32, _f32, _f32,
                                 _vp]),
@@ -93,16 +93,16 @@ def tc_embed_forward(W, table_row_offset, num_tables, bags_per_table, indices, b
         _ptr(out, torch.float32, "out"), _stream(stream)), "tc_embed_forward")
 
 
-def tc_cast_workspace_bytes(num_pairs: int, total_rows: int) -> int:
-    return int(_lib.tc_cast_workspace_bytes(num_pairs, total_rows))
+def tc_cast_workspace_bytes(num_pairs: int, total_rows: int, num_tables: int) -> int:
+    return int(_lib.tc_cast_workspace_bytes(num_pairs, total_rows, num_tables))
 
 
-def tc_cast_index(table_row_offset, num_tables, bags_per_table, total_rows, indices, bag_offsets,
-                  num_pairs, unique_rows, seg_offsets, casted_src, casted_dst, num_unique,
-                  workspace, stream=None) -> None:
+def tc_cast_index(table_row_offset, num_tables, bags_per_table, total_rows, max_table_rows,
+                  indices, bag_offsets, num_pairs, unique_rows, seg_offsets, casted_src,
+                  casted_dst, num_unique, workspace, stream=None) -> None:
     _check(_lib.tc_cast_index(
         _ptr(table_row_offset, torch.int64, "table_row_offset"), num_tables, bags_per_table,
-        total_rows, _ptr(indices, torch.int32, "indices"),
+        total_rows, max_table_rows, _ptr(indices, torch.int32, "indices"),
         _ptr(bag_offsets, torch.int32, "bag_offsets"), num_pairs,
         _ptr(unique_rows, torch.int32, "unique_rows"), _ptr(seg_offsets, torch.int32, "seg_offsets"),
         _ptr(casted_src, torch.int32, "casted_src"), _ptr(casted_dst, torch.int32, "casted_dst"),
@@ -138,11 +138,12 @@ class EmbeddingTrainer:
 
     def __init__(self, *, total_rows: int, dim: int, num_tables: int, bags_per_table: int,
                  max_pairs: int, optimizer: str = "sgd", lr: float = 0.01, eps: float = 1e-8,
-                 device="cuda", table: torch.Tensor | None = None):
+                 device="cuda", table: torch.Tensor | None = None, max_table_rows: int = 0):
         self.total_rows, self.dim = total_rows, dim
         self.num_tables, self.bags_per_table = num_tables, bags_per_table
         self.num_bags = num_tables * bags_per_table
         self.max_pairs = max_pairs
+        self.max_table_rows = max_table_rows
         self.max_unique = min(max_pairs, total_rows)
         self.opt_kind = OPTIMIZERS[optimizer]
         self.lr, self.eps = lr, eps
@@ -157,7 +158,7 @@ class EmbeddingTrainer:
         self.casted_dst = torch.empty(max(max_pairs, 1), **i32)
         self.num_unique = torch.zeros(1, **i32)
         self.coal = torch.empty((max(self.max_unique, 1), dim), dtype=torch.float32, device=device)
-        ws = tc_cast_workspace_bytes(max_pairs, total_rows)
+        ws = tc_cast_workspace_bytes(max_pairs, total_rows, num_tables)
         self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=device)
 
     def forward(self, table_row_offset, indices, bag_offsets, stream=None):
@@ -167,8 +168,8 @@ class EmbeddingTrainer:
     def cast(self, table_row_offset, indices, bag_offsets, num_pairs, stream=None,
              with_casted_dst=False):
         tc_cast_index(table_row_offset, self.num_tables, self.bags_per_table, self.total_rows,
-                      indices, bag_offsets, num_pairs, self.unique_rows, self.seg_offsets,
-                      self.casted_src, self.casted_dst if with_casted_dst else None,
+                      self.max_table_rows, indices, bag_offsets, num_pairs, self.unique_rows,
+                      self.seg_offsets, self.casted_src, self.casted_dst if with_casted_dst else None,
                       self.num_unique, self.workspace, stream)
 
     def backward(self, grad_out, stream=None):

@@ -44,12 +44,16 @@ def to_dev(a: np.ndarray) -> torch.Tensor:
 class GpuRun:
     """A trainer plus device copies of its batches."""
 
-    def __init__(self, w: wl.Workload, max_pairs: int, fill_on_device=True, table=None):
+    def __init__(self, w: wl.Workload, max_pairs: int, fill_on_device=True, table=None,
+                 max_table_rows=None):
+        """max_table_rows: the cast's table-size bound (None: rows per table,
+        which sorts on table-local rows; 0: global rows)."""
         self.w = w
         self.trainer = tc.EmbeddingTrainer(
             total_rows=w.total_rows, dim=w.dim, num_tables=w.num_tables,
             bags_per_table=w.batch, max_pairs=max_pairs, optimizer=w.optimizer, lr=w.lr,
-            eps=w.eps)
+            eps=w.eps,
+            max_table_rows=w.rows_per_table if max_table_rows is None else max_table_rows)
         if table is not None:
             self.trainer.W.copy_(torch.from_numpy(table))
         elif fill_on_device:

@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(header):
 
 
 def test_version_and_status_strings(tc):
-    assert tc.tc_abi_version() == 1
+    assert tc.tc_abi_version() == 2
     lib = tc._lib
     for code, name in enumerate(["TC_OK", "TC_ERR_INVALID_ARG", "TC_ERR_UNSUPPORTED",
                                  "TC_ERR_WORKSPACE", "TC_ERR_HIP"]):
@@ -47,8 +47,8 @@ def test_version_and_status_strings(tc):
 
 def test_workspace_bytes(tc):
     lib = tc._lib
-    assert lib.tc_cast_workspace_bytes(-1, 10) == 0
-    sizes = [lib.tc_cast_workspace_bytes(n, 1000) for n in (0, 1, 4096, 4097, 10 ** 6)]
+    assert lib.tc_cast_workspace_bytes(-1, 10, 1) == 0
+    sizes = [lib.tc_cast_workspace_bytes(n, 1000, 4) for n in (0, 1, 4096, 4097, 10 ** 6)]
     assert sizes == sorted(sizes)
     assert sizes[-1] >= 16 * 10 ** 6   # four int32 arrays of num_pairs
     assert all(s % 256 == 0 for s in sizes)
@@ -108,12 +108,13 @@ def test_forward_rejects_bad_arguments(tc):
 
 def test_cast_rejects_bad_arguments(tc):
     lib, h = tc._lib, HostBuffers()
-    need = lib.tc_cast_workspace_bytes(1000, 100)
+    need = lib.tc_cast_workspace_bytes(1000, 100, 1)
 
     def f(**k):
         return lib.tc_cast_index(
             k.get("off", h.lp()), k.get("T", 1), k.get("B", 50), k.get("rows", 100),
-            k.get("idx", h.ip()), k.get("bo", h.ip()), k.get("n", 1000), k.get("ur", h.ip()),
+            k.get("mtr", 100), k.get("idx", h.ip()), k.get("bo", h.ip()), k.get("n", 1000),
+            k.get("ur", h.ip()),
             k.get("so", h.ip()), k.get("cs", h.ip()), k.get("cd", None), k.get("nu", h.ip()),
             k.get("ws", h.wsp()), k.get("wsb", need), None)
     assert f(wsb=need - 1) == tc.TC_ERR_WORKSPACE and "workspace" in _err(tc)
@@ -122,6 +123,7 @@ def test_cast_rejects_bad_arguments(tc):
     assert f(n=-5) == tc.TC_ERR_INVALID_ARG
     assert f(n=2 ** 31) == tc.TC_ERR_INVALID_ARG
     assert f(rows=2 ** 31) == tc.TC_ERR_INVALID_ARG
+    assert f(mtr=-1) == tc.TC_ERR_INVALID_ARG
     assert f(cs=None) == tc.TC_ERR_INVALID_ARG
     assert f(ur=None) == tc.TC_ERR_INVALID_ARG
     assert f(nu=None) == tc.TC_ERR_INVALID_ARG

@@ -1,0 +1,118 @@
+"""tc_cast_index under table layouts the workloads do not cover, against the
+CPU oracle's Tensor Casting (Algorithm 2): tables of very different sizes,
+tables without pairs, per-table pair counts at and around the sort tile
+(2048 pairs), more tables than the table-local sort handles (global-row
+fallback), and the same batch cast with and without a table-size bound.
+Index outputs must be bit-exact in every case."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2010_13100_amd import tc
+
+pytestmark = pytest.mark.gpu
+
+TILE = 2048
+
+
+def make_case(table_rows, pairs_per_table, bags_per_table, seed):
+    """CSR batch: table t gets pairs_per_table[t] pairs spread over its bags,
+    indices uniform over its rows (with skew toward a few rows)."""
+    rng = np.random.default_rng(seed)
+    T = len(table_rows)
+    off = np.zeros(T + 1, np.int64)
+    np.cumsum(table_rows, out=off[1:])
+    lengths, flat = [], []
+    for t in range(T):
+        n = pairs_per_table[t]
+        cuts = np.sort(rng.integers(0, n + 1, size=bags_per_table - 1)) if n else \
+            np.zeros(bags_per_table - 1, np.int64)
+        ln = np.diff(np.concatenate([[0], cuts, [n]]))
+        lengths.extend(ln.tolist())
+        hot = rng.integers(0, table_rows[t], size=4)
+        idx = np.where(rng.random(n) < 0.3, hot[rng.integers(0, 4, size=n)],
+                       rng.integers(0, table_rows[t], size=n)) if n else np.zeros(0, np.int64)
+        flat.append(idx)
+    bo = np.zeros(len(lengths) + 1, np.int64)
+    np.cumsum(lengths, out=bo[1:])
+    indices = np.concatenate(flat).astype(np.int32) if flat else np.zeros(0, np.int32)
+    return off, bo.astype(np.int32), indices
+
+
+def oracle_cast(off, bo, indices, bags_per_table):
+    orc = oracle.Oracle("f32")
+    T = len(off) - 1
+    src, dst = orc.pairs_from_csr(T, bags_per_table, off, indices, bo)
+    return orc.tensor_casting(src, dst)
+
+
+def gpu_cast(off, bo, indices, bags_per_table, max_table_rows):
+    T = len(off) - 1
+    total_rows = int(off[-1])
+    n = len(indices)
+    dev = torch.device("cuda", 0)
+    i32 = dict(dtype=torch.int32, device=dev)
+    cap = max(min(n, total_rows), 1)
+    ur = torch.full((cap,), -7, **i32)
+    so = torch.full((cap + 1,), -7, **i32)
+    cs = torch.full((max(n, 1),), -7, **i32)
+    cd = torch.full((max(n, 1),), -7, **i32)
+    nu = torch.zeros(1, **i32)
+    ws = torch.empty(max(tc.tc_cast_workspace_bytes(n, total_rows, T), 256), dtype=torch.uint8,
+                     device=dev)
+    tc.tc_cast_index(torch.from_numpy(off).to(dev), T, bags_per_table, total_rows,
+                     max_table_rows, torch.from_numpy(indices).to(dev) if n else cs,
+                     torch.from_numpy(bo).to(dev), n, ur, so, cs, cd, nu, ws)
+    torch.cuda.synchronize()
+    u = int(nu.item())
+    return dict(num_unique=u, unique_rows=ur[:u].cpu().numpy(),
+                seg_offsets=so[:u + 1].cpu().numpy(), casted_src=cs[:n].cpu().numpy(),
+                casted_dst=cd[:n].cpu().numpy())
+
+
+def check(name, table_rows, pairs_per_table, bags_per_table=5, seed=0, bounds=None):
+    off, bo, indices = make_case(table_rows, pairs_per_table, bags_per_table, seed)
+    print(f"\n[{name}] tables {len(table_rows)} pairs {len(indices)}", flush=True)
+    ref = oracle_cast(off, bo, indices, bags_per_table)
+    n = len(indices)
+    for bound in (bounds if bounds is not None else [max(table_rows), 0]):
+        got = gpu_cast(off, bo, indices, bags_per_table, bound)
+        assert got["num_unique"] == ref["num_unique"], bound
+        assert np.array_equal(got["unique_rows"], ref["unique_rows"]), bound
+        assert np.array_equal(got["seg_offsets"], ref["seg_offsets"]), bound
+        assert np.array_equal(got["casted_src"], ref["casted_src"][:n]), bound
+        assert np.array_equal(got["casted_dst"], ref["casted_dst"][:n]), bound
+
+
+def test_unequal_tables():
+    check("unequal", [5, 1000, 3, 70000, 129], [40, 3000, 7, 9000, 2500])
+
+
+def test_tables_without_pairs():
+    check("empty tables", [300, 400, 500, 600, 700], [0, 2500, 0, 0, 10])
+
+
+def test_per_table_counts_at_tile_edges():
+    counts = [TILE - 1, TILE, TILE + 1, 2 * TILE, 1, 3 * TILE - 1]
+    check("tile edges", [4096] * len(counts), counts, bags_per_table=7, seed=3)
+
+
+def test_many_tables_use_global_rows():
+    # more tables than the table-local sort handles: one segment of global rows
+    T = 300
+    rng = np.random.default_rng(5)
+    check("300 tables", rng.integers(1, 50, size=T).tolist(),
+          rng.integers(0, 40, size=T).tolist(), bags_per_table=3, seed=5)
+
+
+def test_bound_variants_agree():
+    # bounds: exact, loose but still saving bits, no saving (= total rows), none
+    rows = [2 ** 15] * 16
+    check("bounds", rows, [5000] * 16, bags_per_table=64, seed=7,
+          bounds=[2 ** 15, 2 ** 16 + 5, 16 * 2 ** 15, 0])
+
+
+def test_single_table_and_keys_of_one_bit():
+    check("one table", [2], [9000], bags_per_table=11, seed=9)
+    check("rows of one", [1, 1, 1], [3000, 1, 2049], bags_per_table=2, seed=11)

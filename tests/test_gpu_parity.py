@@ -14,7 +14,7 @@ pytestmark = pytest.mark.gpu
 
 W = wl.WORKLOADS
 # Each workload's distributions at sizes the oracle finishes in seconds; the
-# pair counts span several 4096-pair sort tiles and end in a ragged tile.
+# pair counts span several 2048-pair sort tiles and end in a ragged tile.
 SMALL = {
     "c1": W["c1"],
     "c2-2x20k": W["c2"].scaled(name="c2-2x20k", num_tables=2, rows_per_table=20_000, batch=256),
@@ -29,13 +29,18 @@ def global_rows(w, b):
     return b.table_row_offset[t] + b.indices
 
 
+@pytest.mark.parametrize("bound", ["table-local", "global"])
 @pytest.mark.parametrize("name", list(SMALL))
-def test_two_steps_match_oracle(name):
+def test_two_steps_match_oracle(name, bound):
+    """bound: the cast sorts on table-local rows (the table size is passed as
+    the bound) or on global rows (no bound)."""
     w = SMALL[name]
     batches = [wl.make_batch(w, s) for s in (0, 1)]
     touched = np.unique(np.concatenate([global_rows(w, b) for b in batches]))
-    print(f"\n[{name}] pairs {[b.num_pairs for b in batches]} touched {len(touched)}", flush=True)
-    run = GpuRun(w, max_pairs=max(b.num_pairs for b in batches))
+    print(f"\n[{name} {bound}] pairs {[b.num_pairs for b in batches]} touched {len(touched)}",
+          flush=True)
+    run = GpuRun(w, max_pairs=max(b.num_pairs for b in batches),
+                 max_table_rows=None if bound == "table-local" else 0)
     model = OracleModel(w, touched)
     for b in batches:
         out, cast, coal = run.step(b)
