@@ -1,10 +1,12 @@
 """Benchmark one sparse-embedding training step on one MI355X.
 
 A step is the whole hot path on one synthetic batch: tc_embed_forward,
-tc_cast_index, tc_embed_backward and tc_sparse_update, back to back on one
-stream, with inputs already resident in HBM. Prints ONE JSON line.
+tc_cast_index, then tc_embed_backward_update (the casted backward and the
+sparse update in one pass; --unfused calls tc_embed_backward and
+tc_sparse_update instead), back to back on one stream, with inputs already
+resident in HBM. Prints ONE JSON line.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config c2]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config c2] [--unfused]
 
 Default workload: 8 tables x 1M rows x 64 fp32, batch 2048, 80 Zipf(1.05)
 indices per bag, SGD (configuration "c2"). Other configurations: c1..c5.
@@ -32,19 +34,24 @@ def algorithmic_bytes(w, n, u, nbags):
     bwd = n * 4 + (u + 1) * 4 + n * D4 + u * D4
     rows_rw = 3 if w.optimizer == "sgd" else 5   # G, W in, W out (+ A in, A out)
     upd = u * 4 + rows_rw * u * D4
-    return {"forward": fwd, "cast": cast, "backward": bwd, "update": upd}
+    # fused: the coalesced rows stay in registers (no G written, no G read)
+    fused = n * 4 + (u + 1) * 4 + n * D4 + u * 4 + (rows_rw - 1) * u * D4
+    return {"forward": fwd, "cast": cast, "backward": bwd, "update": upd,
+            "backward_update": fused}
 
 
 # Sources of each call's kernels, and the kernels one call launches.
 KERNEL_SOURCES = {
     "forward": ["tc_internal.h", "tc_group_sum.h", "tc_gather_reduce.hip"],
-    "backward": ["tc_internal.h", "tc_group_sum.h", "tc_backward.hip"],
-    "update": ["tc_internal.h", "tc_update.hip"],
+    "backward": ["tc_internal.h", "tc_group_sum.h", "tc_optim.h", "tc_backward.hip"],
+    "backward_update": ["tc_internal.h", "tc_group_sum.h", "tc_optim.h", "tc_backward.hip"],
+    "update": ["tc_internal.h", "tc_optim.h", "tc_update.hip"],
     "cast": ["tc_internal.h", "tc_cast.hip"],
 }
 KERNEL_NAMES = {
     "forward": ["k_forward"],
     "backward": ["k_backward_long", "k_backward_short"],
+    "backward_update": ["k_backward_long", "k_backward_short"],
     "update": ["k_sparse_update"],
     "cast": ["k_build_keys", "k_radix_hist", "k_radix_scan", "k_radix_scatter", "k_seg_count",
              "k_seg_scan", "k_seg_write"],
@@ -166,6 +173,8 @@ def main():
     ap.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle work for cpu_baseline (0 disables)")
+    ap.add_argument("--unfused", action="store_true",
+                    help="backward and update as two calls (tc_embed_backward, tc_sparse_update)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run 5 plain device copies of BYTES bytes (scale for the HBM "
                          "byte counters) and exit")
@@ -213,11 +222,13 @@ def main():
                  grad=torch.from_numpy(b.grad_out).to(dev), n=b.num_pairs) for b in batches]
     stream = torch.cuda.current_stream(dev)
 
-    calls = ["forward", "cast", "backward", "update"]
+    calls = (["forward", "cast", "backward", "update"] if args.unfused
+             else ["forward", "cast", "backward_update"])
     fns = {"forward": lambda d: trainer.forward(d["off"], d["idx"], d["bo"], stream),
            "cast": lambda d: trainer.cast(d["off"], d["idx"], d["bo"], d["n"], stream),
            "backward": lambda d: trainer.backward(d["grad"], stream),
-           "update": lambda d: trainer.update(stream)}
+           "update": lambda d: trainer.update(stream),
+           "backward_update": lambda d: trainer.backward_update(d["grad"], stream)}
 
     def step(i, ev=None):
         """One step on batch i % NUM_BATCHES. ev: dict call -> (start, stop)
@@ -244,8 +255,8 @@ def main():
     skip = 1 if args.warmup > 1 else 0   # the first step also pays one-time costs
     per_call_ms = {c: float(np.mean([e[c][0].elapsed_time(e[c][1]) for e in wev[skip:]]))
                    for c in calls} if args.warmup else {c: float("nan") for c in calls}
-    single = ["forward", "backward", "update"]
-    dom = max(single, key=lambda c: per_call_ms[c]) if args.warmup else "backward"
+    single = [c for c in calls if c != "cast"]
+    dom = max(single, key=lambda c: per_call_ms[c]) if args.warmup else single[-1]
 
     # timed steps: start/stop around the whole region, one event pair around
     # the dominant call of each step (on the stream its kernels run on)
@@ -275,7 +286,8 @@ def main():
     for i in range(args.steps):
         b = (args.warmup + i) % NUM_BATCHES
         for c, v in algorithmic_bytes(w, dbat[b]["n"], uniq[b], w.num_bags).items():
-            nbytes[c] += v / args.steps
+            if c in nbytes:
+                nbytes[c] += v / args.steps
     step_bytes = sum(nbytes.values())
 
     achieved = nbytes[dom] / (dom_ms * 1e-3) / 1e9
@@ -299,7 +311,8 @@ def main():
                    "rows_per_table": w.rows_per_table, "dim": w.dim, "batch": w.batch,
                    "pairs_per_step": round(float(np.mean([d["n"] for d in dbat])), 1),
                    "unique_rows_per_step": round(float(np.mean(uniq)), 1),
-                   "optimizer": w.optimizer},
+                   "optimizer": w.optimizer,
+                   "step_calls": calls},
         "step_algorithmic_GBps": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
         "step_algorithmic_frac_of_hbm_peak": round(step_bytes / (ms_step * 1e-3) / 1e9
                                                    / HBM_PEAK_GBS, 4),

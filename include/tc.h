@@ -11,6 +11,9 @@
  *   tc_embed_backward  casted gradient gather-reduce (Algorithm 3)
  *   tc_sparse_update   gradient scatter with SGD or Adagrad (Sec. II-B, Eq. 2)
  *
+ * tc_embed_backward_update does the last two in one pass (same results bit
+ * for bit) without storing the coalesced gradient in device memory.
+ *
  * Conventions shared by every call
  * --------------------------------
  * Pointers are DEVICE pointers owned by the caller unless a comment says
@@ -163,6 +166,23 @@ tc_status tc_sparse_update(float *W, float *opt_state, int64_t total_rows, int32
                            const int32_t *unique_rows, const float *coal_grad,
                            const int32_t *num_unique, int64_t max_unique, int32_t opt_kind,
                            float lr, float eps, hipStream_t stream);
+
+/*
+ * Casted gradient gather-reduce (Algorithm 3) fused with the gradient
+ * scatter + optimizer (Sec. II-B, Eq. 2): for every u < *num_unique, the
+ * coalesced row G of tc_embed_backward is formed in registers and applied to
+ * W[unique_rows[u]] (and the Adagrad accumulator) exactly as
+ * tc_sparse_update applies it. The results equal those two calls bit for
+ * bit; the coalesced gradient is stored to coal_grad only if that is not
+ * NULL. Arguments are those of the two calls (coal_grad optional); W,
+ * opt_state and grad_out must not overlap.
+ */
+tc_status tc_embed_backward_update(const float *grad_out, int32_t num_bags, int32_t dim,
+                                   const int32_t *seg_offsets, const int32_t *casted_src,
+                                   const int32_t *unique_rows, const int32_t *num_unique,
+                                   int64_t max_unique, float *W, float *opt_state,
+                                   int64_t total_rows, int32_t opt_kind, float lr, float eps,
+                                   float *coal_grad, hipStream_t stream);
 
 /* Static text for a status code. */
 const char *tc_status_string(tc_status status);

@@ -17,9 +17,16 @@
 //
 // The long kernel is launched first; both only read their inputs and write
 // disjoint rows of coal_grad. No atomics anywhere.
+//
+// Fused with the update (tc_embed_backward_update), the owner of coalesced
+// row u applies the optimizer step to table row unique_rows[u] straight from
+// its registers (tc_optim.h, the arithmetic of tc_sparse_update), so the
+// coalesced rows need not go through HBM; unique rows are distinct, so every
+// table row still has a single writer.
 #include <type_traits>
 
 #include "tc_group_sum.h"
+#include "tc_optim.h"
 
 namespace tc {
 namespace {
@@ -41,9 +48,9 @@ constexpr int kLoadsPerChunk = kChunkRows / kRowsPerLoad;  // 16
 // Chunks whose row loads (kAhead) and id loads (kIdAhead) a producer keeps in
 // flight; the producer code is unrolled over kPeriod chunks so that every ring
 // slot is a fixed register.
-constexpr int kAhead = 6;
-constexpr int kIdAhead = 12;
-constexpr int kPeriod = 12;
+constexpr int kAhead = 3;
+constexpr int kIdAhead = 6;
+constexpr int kPeriod = 6;
 static_assert(kPeriod % kAhead == 0 && kPeriod % kIdAhead == 0 && kPeriod % kBuffers == 0,
               "ring periods must divide kPeriod");
 // Ranges of segments scanned by the blocks of the long kernel (per part).
@@ -60,6 +67,69 @@ constexpr int32_t kOutOfRange = 0x7ffff000;
 // rows 4k..4k+3 sits at group position k ^ swz(c); the swizzle spreads both
 // the consumer's 16-byte reads (16 neighbouring columns, same k) and the
 // producers' 4-byte writes (16 columns 4 apart, same k) over distinct banks.
+// What becomes of a coalesced row: stored to coal (if not null) and/or
+// applied to W[rows[u]] (if W is not null) with optimizer `kind`.
+struct RowSink {
+    float *coal;
+    float *W;
+    float *A;  // Adagrad accumulator
+    const int32_t *rows;
+    int32_t kind;
+    float lr, eps;
+};
+
+// One lane's column `col` of coalesced row u.
+__device__ __forceinline__ void sink_value(const RowSink &k, int64_t u, int32_t dim, int32_t col,
+                                           float g) {
+    if (k.coal) k.coal[u * dim + col] = g;
+    if (k.W) {
+        const int64_t at = int64_t(k.rows[u]) * dim + col;
+        float w = k.W[at];
+        if (k.kind == TC_OPT_SGD) {
+            w = sgd_step(w, g, k.lr);
+        } else {
+            float a = k.A[at];
+            adagrad_step(w, a, g, k.lr, k.eps);
+            k.A[at] = a;
+        }
+        k.W[at] = w;
+    }
+}
+
+// A lane group's float4 chunks of coalesced row u.
+template <int LANES, int CHUNKS>
+__device__ __forceinline__ void sink_group(const RowSink &k, int64_t u, int32_t dim, int sub,
+                                           const float4 (&acc)[CHUNKS]) {
+    if (k.coal) group_store<LANES, CHUNKS>(k.coal + u * dim, dim, sub, acc);
+    if (k.W) {
+        const int d4 = dim >> 2;
+        const int64_t r = k.rows[u];
+        float *wrow = k.W + r * dim;
+#pragma unroll
+        for (int c = 0; c < CHUNKS; ++c) {
+            const int col4 = sub + c * LANES;
+            if (col4 >= d4) continue;
+            const float4 g = acc[c];
+            float4 w = *reinterpret_cast<const float4 *>(wrow + 4 * col4);
+            if (k.kind == TC_OPT_SGD) {
+                w.x = sgd_step(w.x, g.x, k.lr);
+                w.y = sgd_step(w.y, g.y, k.lr);
+                w.z = sgd_step(w.z, g.z, k.lr);
+                w.w = sgd_step(w.w, g.w, k.lr);
+            } else {
+                float *arow = k.A + r * dim;
+                float4 a = *reinterpret_cast<const float4 *>(arow + 4 * col4);
+                adagrad_step(w.x, a.x, g.x, k.lr, k.eps);
+                adagrad_step(w.y, a.y, g.y, k.lr, k.eps);
+                adagrad_step(w.z, a.z, g.z, k.lr, k.eps);
+                adagrad_step(w.w, a.w, g.w, k.lr, k.eps);
+                *reinterpret_cast<float4 *>(arow + 4 * col4) = a;
+            }
+            *reinterpret_cast<float4 *>(wrow + 4 * col4) = w;
+        }
+    }
+}
+
 struct LongLds {
     alignas(16) float cols[kBuffers][kPartCols][kChunkRows];
     int32_t offs[kProducers][kChunkRows];
@@ -140,17 +210,14 @@ __device__ void long_producer(LongLds &lds, __amdgpu_buffer_rsrc_t id_rsrc, int3
     };
 #pragma unroll
     for (int e = 0; e < kIdAhead; ++e) iv[e] = load_ids(e);
-    static_assert(kAhead == 6, "the prologue issues kAhead chunks");
+    static_assert(kAhead == 3, "the prologue issues kAhead chunks");
     issue(Int<0>{}, Int<0>{}, 0);
     issue(Int<1>{}, Int<1>{}, 1);
     issue(Int<2>{}, Int<2>{}, 2);
-    issue(Int<3>{}, Int<3>{}, 3);
-    issue(Int<4>{}, Int<4>{}, 4);
-    issue(Int<5>{}, Int<5>{}, 5);
     write(Int<0>{}, Int<0>{});
-    issue(Int<0>{}, Int<6>{}, 6);
+    issue(Int<0>{}, Int<3>{}, 3);
     write(Int<1>{}, Int<1>{});
-    issue(Int<1>{}, Int<7>{}, 7);
+    issue(Int<1>{}, Int<4>{}, 4);
     lds_barrier();
     // Step i: write chunk i + 2, refill its registers with chunk i + 2 + kAhead.
     auto step = [&](auto ms, int32_t i) {
@@ -162,7 +229,7 @@ __device__ void long_producer(LongLds &lds, __amdgpu_buffer_rsrc_t id_rsrc, int3
     // Whole periods in a loop with a single exit (a loop left from the middle
     // merges the load bookkeeping of every exit at its head, which costs a
     // full wait), then the remaining steps once.
-    static_assert(kPeriod == 12, "the step loop is unrolled over 12 chunks");
+    static_assert(kPeriod == 6, "the step loop is unrolled over 6 chunks");
     int32_t i = 0;
     const int32_t periods = nchunks / kPeriod;
     for (int32_t k = 0; k < periods; ++k, i += kPeriod) {
@@ -172,12 +239,6 @@ __device__ void long_producer(LongLds &lds, __amdgpu_buffer_rsrc_t id_rsrc, int3
         step(Int<3>{}, i + 3);
         step(Int<4>{}, i + 4);
         step(Int<5>{}, i + 5);
-        step(Int<6>{}, i + 6);
-        step(Int<7>{}, i + 7);
-        step(Int<8>{}, i + 8);
-        step(Int<9>{}, i + 9);
-        step(Int<10>{}, i + 10);
-        step(Int<11>{}, i + 11);
     }
     const int32_t rem = nchunks - i;
     if (rem > 0) { step(Int<0>{}, i);
@@ -185,61 +246,55 @@ __device__ void long_producer(LongLds &lds, __amdgpu_buffer_rsrc_t id_rsrc, int3
     if (rem > 2) { step(Int<2>{}, i + 2);
     if (rem > 3) { step(Int<3>{}, i + 3);
     if (rem > 4) { step(Int<4>{}, i + 4);
-    if (rem > 5) { step(Int<5>{}, i + 5);
-    if (rem > 6) { step(Int<6>{}, i + 6);
-    if (rem > 7) { step(Int<7>{}, i + 7);
-    if (rem > 8) { step(Int<8>{}, i + 8);
-    if (rem > 9) { step(Int<9>{}, i + 9);
-    if (rem > 10) { step(Int<10>{}, i + 10);
-    }}}}}}}}}}}
+    }}}}}
 }
 
 // The consumer: lane l owns column l of the part and adds the rows of chunk
-// i in order, 64 per step, four rows per 16-byte LDS read. Chunk i + 1 is
-// complete in LDS during step i (it was written one step ahead), so step i
-// reads it into registers between the adds of chunk i and the chain never
-// waits for LDS. Executes exactly 1 + nchunks barriers, as the producers do.
+// i in order, 64 per step, four rows per 16-byte LDS read. Reads run kAheadG
+// groups (4 rows each) ahead of the adds through a small register ring; chunk
+// i + 1 is complete in LDS during step i (it was written one step ahead), so
+// the read-ahead crosses into it freely and the chain never waits for LDS.
+// Executes exactly 1 + nchunks barriers, as the producers do.
+constexpr int kAheadG = 8;
 __device__ float long_consumer(LongLds &lds, int32_t nchunks) {
     constexpr int G = kChunkRows / 4;
+    static_assert(G % kAheadG == 0, "ring slots repeat every step");
     const int lane = threadIdx.x & (kWave - 1);
     const char *lds_cols = reinterpret_cast<const char *>(&lds.cols[0][0][0]);
     int32_t rpos[G];  // byte offset of rows 4k..4k+3 of this lane's column
 #pragma unroll
     for (int k = 0; k < G; ++k) rpos[k] = lds_pos(4 * k, lane);
+    auto read = [&](int b, int k) -> float4 {
+        return *reinterpret_cast<const float4 *>(lds_cols + b * kBufferBytes + rpos[k]);
+    };
     float acc = 0.f;
     lds_barrier();
-    float4 xa[G], xb[G];
+    float4 ring[kAheadG];
 #pragma unroll
-    for (int k = 0; k < G; ++k) xa[k] = *reinterpret_cast<const float4 *>(lds_cols + rpos[k]);
-    // adds cur (chunk i) while reading chunk i + 1 from buffer B into nxt
-    auto step = [&](auto bs, const float4(&cur)[G], float4(&nxt)[G]) {
-        constexpr int B = decltype(bs)::value;
+    for (int k = 0; k < kAheadG; ++k) ring[k] = read(0, k);
+    // step i: chunk i sits in buffer B = i % 3, chunk i + 1 in (B + 1) % 3
+    auto step = [&](auto bs) {
+        constexpr int B = decltype(bs)::value, BN = (B + 1) % kBuffers;
 #pragma unroll
         for (int k = 0; k < G; ++k) {
-            nxt[k] = *reinterpret_cast<const float4 *>(lds_cols + B * kBufferBytes + rpos[k]);
-            acc = acc + cur[k].x;
-            acc = acc + cur[k].y;
-            acc = acc + cur[k].z;
-            acc = acc + cur[k].w;
+            const float4 x = ring[k % kAheadG];
+            ring[k % kAheadG] = k + kAheadG < G ? read(B, k + kAheadG) : read(BN, k + kAheadG - G);
+            acc = acc + x.x;
+            acc = acc + x.y;
+            acc = acc + x.z;
+            acc = acc + x.w;
             __builtin_amdgcn_sched_barrier(0);
         }
         lds_barrier();
     };
-    // step i reads buffer (i + 1) % 3 into the other register set: period 6
     int32_t i = 0;
     for (;;) {
         if (i >= nchunks) break;
-        step(Int<1>{}, xa, xb);
+        step(Int<0>{});
         if (++i >= nchunks) break;
-        step(Int<2>{}, xb, xa);
+        step(Int<1>{});
         if (++i >= nchunks) break;
-        step(Int<0>{}, xa, xb);
-        if (++i >= nchunks) break;
-        step(Int<1>{}, xb, xa);
-        if (++i >= nchunks) break;
-        step(Int<2>{}, xa, xb);
-        if (++i >= nchunks) break;
-        step(Int<0>{}, xb, xa);
+        step(Int<2>{});
         ++i;
     }
     return acc;
@@ -253,7 +308,7 @@ __device__ float long_consumer(LongLds &lds, int32_t nchunks) {
 __global__ __launch_bounds__(kLongThreads) void k_backward_long(
     const float *__restrict__ grad, int32_t dim, const int32_t *__restrict__ ids,
     const int32_t *__restrict__ offsets, const int32_t *__restrict__ num_out_dev,
-    int64_t num_out_cap, float *__restrict__ out) {
+    int64_t num_out_cap, RowSink sink) {
     __shared__ LongLds lds;
     const int lane = threadIdx.x & (kWave - 1);
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -288,7 +343,6 @@ __global__ __launch_bounds__(kLongThreads) void k_backward_long(
                 const int32_t beg = __builtin_amdgcn_readlane(o0, j);
                 const int32_t len = __builtin_amdgcn_readlane(o1, j) - beg;
                 const int64_t seg = c0 + int64_t(kWave) * i + j;
-                float *out_row = out + seg * int64_t(dim);
                 const int32_t *sid = ids + beg;
                 // ids within a segment are non-decreasing (stable cast order)
                 const int32_t first = __builtin_amdgcn_readfirstlane(sid[0]);
@@ -303,7 +357,7 @@ __global__ __launch_bounds__(kLongThreads) void k_backward_long(
                         const float *colp = grad + (col < dim ? col : dim - 1);
                         for (int32_t k = 0; k < len; ++k)
                             acc = acc + colp[int64_t(sid[k]) * dim];
-                        if (col < dim) out_row[col] = acc;
+                        if (col < dim) sink_value(sink, seg, dim, col, acc);
                     }
                     continue;
                 }
@@ -316,7 +370,7 @@ __global__ __launch_bounds__(kLongThreads) void k_backward_long(
                 const int32_t part_bytes = part * kPartCols * 4;
                 if (w == 0) {
                     const float acc = long_consumer(lds, nchunks);
-                    if (col < dim) out_row[col] = acc;
+                    if (col < dim) sink_value(sink, seg, dim, col, acc);
                 } else if (w == 1) {
                     long_producer<0>(lds, id_rsrc, len, first, row_bytes, part_bytes, nchunks, rsrc);
                 } else if (w == 2) {
@@ -337,7 +391,7 @@ template <int LANES, int CHUNKS>
 __global__ __launch_bounds__(kBlock) void k_backward_short(
     const float *__restrict__ grad, int32_t dim, const int32_t *__restrict__ ids,
     const int32_t *__restrict__ offsets, const int32_t *__restrict__ num_out_dev,
-    int64_t num_out_cap, float *__restrict__ out) {
+    int64_t num_out_cap, RowSink sink) {
     constexpr int kGroups = kWave / LANES;
     const int lane = threadIdx.x & (kWave - 1);
     const int sub = lane & (LANES - 1);
@@ -360,13 +414,13 @@ __global__ __launch_bounds__(kBlock) void k_backward_short(
 #pragma unroll
         for (int c = 0; c < CHUNKS; ++c) acc[c] = make_float4(0.f, 0.f, 0.f, 0.f);
         group_range_sum<LANES, CHUNKS>(grad, dim, ids, 0, beg, end, sub, acc);
-        if (mine) group_store<LANES, CHUNKS>(out + o * int64_t(dim), dim, sub, acc);
+        if (mine) sink_group<LANES, CHUNKS>(sink, o, dim, sub, acc);
     }
 }
 
 tc_status launch_backward(const float *grad, int32_t dim, const int32_t *ids,
                           const int32_t *offsets, const int32_t *num_out_dev, int64_t cap,
-                          float *out, hipStream_t stream) {
+                          const RowSink &out, hipStream_t stream) {
     const int parts = (dim + kPartCols - 1) / kPartCols;
     const int ranges = kLongRanges / parts > 64 ? kLongRanges / parts : 64;
     k_backward_long<<<dim3(ranges, parts), kLongThreads, 0, stream>>>(grad, dim, ids, offsets,
@@ -418,6 +472,36 @@ extern "C" tc_status tc_embed_backward(const float *grad_out, int32_t num_bags, 
                TC_ERR_INVALID_ARG, "tc_embed_backward: null pointer");
     TC_REQUIRE(aligned16(grad_out) && aligned16(coal_grad), TC_ERR_UNSUPPORTED,
                "tc_embed_backward: grad_out and coal_grad must be 16-byte aligned");
-    return launch_backward(grad_out, dim, casted_src, seg_offsets, num_unique, max_unique,
-                           coal_grad, stream);
+    const RowSink sink{coal_grad, nullptr, nullptr, nullptr, TC_OPT_SGD, 0.f, 0.f};
+    return launch_backward(grad_out, dim, casted_src, seg_offsets, num_unique, max_unique, sink,
+                           stream);
+}
+
+extern "C" tc_status tc_embed_backward_update(
+    const float *grad_out, int32_t num_bags, int32_t dim, const int32_t *seg_offsets,
+    const int32_t *casted_src, const int32_t *unique_rows, const int32_t *num_unique,
+    int64_t max_unique, float *W, float *opt_state, int64_t total_rows, int32_t opt_kind,
+    float lr, float eps, float *coal_grad, hipStream_t stream) {
+    clear_error();
+    TC_REQUIRE(num_bags >= 0 && max_unique >= 0 && total_rows >= 0, TC_ERR_INVALID_ARG,
+               "tc_embed_backward_update: negative size");
+    TC_REQUIRE(max_unique < (int64_t(1) << 31) && total_rows < (int64_t(1) << 31),
+               TC_ERR_INVALID_ARG, "tc_embed_backward_update: sizes must be below 2^31");
+    TC_REQUIRE(dim > 0 && dim % 4 == 0 && dim <= kMaxDim, TC_ERR_UNSUPPORTED,
+               "tc_embed_backward_update: dim %d must be a multiple of 4 in [4, %d]", dim,
+               kMaxDim);
+    TC_REQUIRE(opt_kind == TC_OPT_SGD || opt_kind == TC_OPT_ADAGRAD, TC_ERR_INVALID_ARG,
+               "tc_embed_backward_update: unknown optimizer %d", opt_kind);
+    TC_REQUIRE((opt_kind == TC_OPT_SGD) == (opt_state == nullptr), TC_ERR_INVALID_ARG,
+               "tc_embed_backward_update: opt_state must be NULL for SGD and given for Adagrad");
+    if (max_unique == 0) return TC_OK;
+    TC_REQUIRE(grad_out && seg_offsets && casted_src && unique_rows && num_unique && W,
+               TC_ERR_INVALID_ARG, "tc_embed_backward_update: null pointer");
+    TC_REQUIRE(aligned16(grad_out) && aligned16(W) && (!opt_state || aligned16(opt_state)) &&
+                   (!coal_grad || aligned16(coal_grad)),
+               TC_ERR_UNSUPPORTED,
+               "tc_embed_backward_update: float pointers must be 16-byte aligned");
+    const RowSink sink{coal_grad, W, opt_state, unique_rows, opt_kind, lr, eps};
+    return launch_backward(grad_out, dim, casted_src, seg_offsets, num_unique, max_unique, sink,
+                           stream);
 }

@@ -4,9 +4,8 @@
 // reads coal_grad[u], reads and writes W[unique_rows[u]] (and the Adagrad
 // accumulator row) with dwordx4 accesses. unique_rows are distinct, so no
 // atomics are needed and the result does not depend on scheduling. The
-// optimizer arithmetic is separately rounded fp32 (the library is built with
-// -ffp-contract=off; division and square root are correctly rounded).
-#include "tc_internal.h"
+// optimizer arithmetic (tc_optim.h) is separately rounded fp32.
+#include "tc_optim.h"
 
 namespace tc {
 namespace {
@@ -39,21 +38,17 @@ __global__ __launch_bounds__(kBlock) void k_sparse_update(
             const float4 g = *reinterpret_cast<const float4 *>(grow + 4 * col4);
             float4 w = *reinterpret_cast<const float4 *>(wrow + 4 * col4);
             if (OPT == TC_OPT_SGD) {
-                w.x = w.x - lr * g.x;
-                w.y = w.y - lr * g.y;
-                w.z = w.z - lr * g.z;
-                w.w = w.w - lr * g.w;
+                w.x = sgd_step(w.x, g.x, lr);
+                w.y = sgd_step(w.y, g.y, lr);
+                w.z = sgd_step(w.z, g.z, lr);
+                w.w = sgd_step(w.w, g.w, lr);
             } else {
                 float *arow = A + r * int64_t(dim);
                 float4 a = *reinterpret_cast<const float4 *>(arow + 4 * col4);
-                a.x = a.x + g.x * g.x;
-                a.y = a.y + g.y * g.y;
-                a.z = a.z + g.z * g.z;
-                a.w = a.w + g.w * g.w;
-                w.x = w.x - lr * (g.x / sqrtf(eps + a.x));
-                w.y = w.y - lr * (g.y / sqrtf(eps + a.y));
-                w.z = w.z - lr * (g.z / sqrtf(eps + a.z));
-                w.w = w.w - lr * (g.w / sqrtf(eps + a.w));
+                adagrad_step(w.x, a.x, g.x, lr, eps);
+                adagrad_step(w.y, a.y, g.y, lr, eps);
+                adagrad_step(w.z, a.z, g.z, lr, eps);
+                adagrad_step(w.w, a.w, g.w, lr, eps);
                 *reinterpret_cast<float4 *>(arow + 4 * col4) = a;
             }
             *reinterpret_cast<float4 *>(wrow + 4 * col4) = w;

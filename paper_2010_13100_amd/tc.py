@@ -29,6 +29,8 @@ _SIGNATURES = {
     "tc_embed_backward": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _i64, _vp, _vp]),
     "tc_sparse_update": (_i32, [_vp, _vp, _i64, _i32, _vp, _vp, _vp, _i64, _i32, _f32, _f32,
                                 _vp]),
+    "tc_embed_backward_update": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _vp,
+                                        _i64, _i32, _f32, _f32, _vp, _vp]),
     "tc_status_string": (ctypes.c_char_p, [_i32]),
     "tc_last_error": (ctypes.c_char_p, []),
     "tc_abi_version": (_i32, []),
@@ -129,6 +131,18 @@ def tc_sparse_update(W, opt_state, unique_rows, coal_grad, num_unique, max_uniqu
         max_unique, opt_kind, lr, eps, _stream(stream)), "tc_sparse_update")
 
 
+def tc_embed_backward_update(grad_out, seg_offsets, casted_src, unique_rows, num_unique,
+                             max_unique, W, opt_state, opt_kind, lr, eps, coal_grad=None,
+                             stream=None) -> None:
+    _check(_lib.tc_embed_backward_update(
+        _ptr(grad_out, torch.float32, "grad_out"), grad_out.shape[0], grad_out.shape[1],
+        _ptr(seg_offsets, torch.int32, "seg_offsets"), _ptr(casted_src, torch.int32, "casted_src"),
+        _ptr(unique_rows, torch.int32, "unique_rows"), _ptr(num_unique, torch.int32, "num_unique"),
+        max_unique, _ptr(W, torch.float32, "W"), _ptr(opt_state, torch.float32, "opt_state"),
+        W.shape[0], opt_kind, lr, eps, _ptr(coal_grad, torch.float32, "coal_grad"),
+        _stream(stream)), "tc_embed_backward_update")
+
+
 class EmbeddingTrainer:
     """Device buffers for one workload shape and the four calls of a step.
 
@@ -180,9 +194,20 @@ class EmbeddingTrainer:
         tc_sparse_update(self.W, self.A, self.unique_rows, self.coal, self.num_unique,
                          self.max_unique, self.opt_kind, self.lr, self.eps, stream)
 
-    def step(self, table_row_offset, indices, bag_offsets, num_pairs, grad_out, stream=None):
-        """forward + cast + backward + update, stream-ordered."""
+    def backward_update(self, grad_out, stream=None, store_coal=False):
+        """backward + update in one pass (coal stored only if store_coal)."""
+        tc_embed_backward_update(grad_out, self.seg_offsets, self.casted_src, self.unique_rows,
+                                 self.num_unique, self.max_unique, self.W, self.A, self.opt_kind,
+                                 self.lr, self.eps, self.coal if store_coal else None, stream)
+
+    def step(self, table_row_offset, indices, bag_offsets, num_pairs, grad_out, stream=None,
+             fused=True):
+        """forward + cast + backward + update, stream-ordered; with fused the
+        last two are one call."""
         self.forward(table_row_offset, indices, bag_offsets, stream)
         self.cast(table_row_offset, indices, bag_offsets, num_pairs, stream)
-        self.backward(grad_out, stream)
-        self.update(stream)
+        if fused:
+            self.backward_update(grad_out, stream)
+        else:
+            self.backward(grad_out, stream)
+            self.update(stream)

@@ -59,15 +59,20 @@ class GpuRun:
         elif fill_on_device:
             device_fill.fill_uniform(self.trainer.W, seed=0, lo=w.init_lo, hi=w.init_hi)
 
-    def run_step(self, b: wl.Batch, with_casted_dst=True):
-        """The four calls on the current stream; outputs stay on the GPU."""
+    def run_step(self, b: wl.Batch, with_casted_dst=True, fused=False, store_coal=True):
+        """The four calls on the current stream (with fused, backward and
+        update as one tc_embed_backward_update call, storing the coalesced
+        rows if store_coal); outputs stay on the GPU."""
         t = self.trainer
         off, idx, bo = to_dev(b.table_row_offset), to_dev(b.indices), to_dev(b.bag_offsets)
         g = to_dev(b.grad_out)
         t.forward(off, idx, bo)
         t.cast(off, idx, bo, b.num_pairs, with_casted_dst=with_casted_dst)
-        t.backward(g)
-        t.update()
+        if fused:
+            t.backward_update(g, store_coal=store_coal)
+        else:
+            t.backward(g)
+            t.update()
         torch.cuda.synchronize()
         self.with_casted_dst = with_casted_dst
         self.n = b.num_pairs
@@ -82,9 +87,9 @@ class GpuRun:
                     casted_dst=(t.casted_dst[:self.n].cpu().numpy() if self.with_casted_dst
                                 else None))
 
-    def step(self, b: wl.Batch, with_casted_dst=True):
+    def step(self, b: wl.Batch, with_casted_dst=True, fused=False):
         """Run a step and fetch everything (small problems only)."""
-        self.run_step(b, with_casted_dst)
+        self.run_step(b, with_casted_dst, fused=fused, store_coal=True)
         cast = self.fetch_cast()
         out = self.trainer.out.cpu().numpy()
         coal = self.trainer.coal[:cast["num_unique"]].cpu().numpy()

@@ -155,6 +155,24 @@ def test_backward_and_update_reject_bad_arguments(tc):
     assert upd(dim=3) == tc.TC_ERR_UNSUPPORTED
     assert upd(ur=None) == tc.TC_ERR_INVALID_ARG
     assert upd(opt=1, A=h.fp(misalign=True)) == tc.TC_ERR_UNSUPPORTED
+
+    def fused(**k):
+        return lib.tc_embed_backward_update(
+            k.get("g", h.fp()), k.get("nb", 10), k.get("dim", 8), k.get("so", h.ip()),
+            k.get("cs", h.ip()), k.get("ur", h.ip()), k.get("nu", h.ip()), k.get("mu", 10),
+            k.get("W", h.fp()), k.get("A", None), k.get("rows", 100), k.get("opt", 0), 0.01, 1e-8,
+            k.get("coal", None), None)
+    assert fused(dim=6) == tc.TC_ERR_UNSUPPORTED
+    assert fused(mu=-1) == tc.TC_ERR_INVALID_ARG
+    assert fused(rows=2 ** 31) == tc.TC_ERR_INVALID_ARG
+    assert fused(A=h.fp()) == tc.TC_ERR_INVALID_ARG             # SGD takes no state
+    assert fused(opt=1) == tc.TC_ERR_INVALID_ARG                # Adagrad needs state
+    assert fused(opt=2, A=h.fp()) == tc.TC_ERR_INVALID_ARG
+    assert fused(W=None) == tc.TC_ERR_INVALID_ARG and "null" in _err(tc)
+    assert fused(ur=None) == tc.TC_ERR_INVALID_ARG
+    assert fused(coal=h.fp(misalign=True)) == tc.TC_ERR_UNSUPPORTED
+    assert fused(W=h.fp(misalign=True)) == tc.TC_ERR_UNSUPPORTED
+    assert fused(mu=0) == tc.TC_OK
     assert h.untouched()
 
 

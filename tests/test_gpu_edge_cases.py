@@ -28,12 +28,20 @@ def custom(num_tables, rows, dim, bags, seed=0, optimizer="sgd"):
 
 
 def check(w, b):
-    print(f"\n[{w.name}] pairs {b.num_pairs}", flush=True)
+    """Both step forms (backward + update as two calls and fused) against the
+    oracle; returns the cast of the fused run."""
+    for fused in (False, True):
+        cast = check_one(w, b, fused)
+    return cast
+
+
+def check_one(w, b, fused):
+    print(f"\n[{w.name} fused={fused}] pairs {b.num_pairs}", flush=True)
     run = GpuRun(w, max_pairs=max(b.num_pairs, 1))
     t = np.repeat(np.arange(w.num_bags) // w.batch, np.diff(b.bag_offsets))
     touched = np.unique(b.table_row_offset[t] + b.indices)
     model = OracleModel(w, touched if len(touched) else np.zeros(1, np.int64))
-    out, cast, coal = run.step(b)
+    out, cast, coal = run.step(b, fused=fused)
     r_out, r_cast, r_coal, _ = model.step(b)
     assert_close(out, r_out, "forward out", bitwise=True)
     compare_cast(cast, r_cast, b.num_pairs)

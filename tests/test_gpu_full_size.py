@@ -1,5 +1,6 @@
 """All five workloads at full size, one step each, in the launch
-configuration the benchmark times. The casted index is compared with the
+configuration the benchmark times (backward and update fused; the coalesced
+rows are also stored, to be checked). The casted index is compared with the
 oracle's in full (bit for bit); forward rows, coalesced gradients and
 updated rows are compared on samples the oracle computes on their own: a
 sampled bag needs only its own pairs, a sampled table row only the pairs
@@ -21,7 +22,7 @@ def test_full_size_step(cfg):
     b = wl.make_batch(w, step=0)
     print(f"\n[{cfg}] {w.name}: {b.num_pairs} pairs", flush=True)
     run = GpuRun(w, max_pairs=b.num_pairs)
-    run.run_step(b, with_casted_dst=True)
+    run.run_step(b, with_casted_dst=True, fused=True, store_coal=True)
     t = run.trainer
     orc = oracle.Oracle("f32")
     src, dst = orc.pairs_from_csr(w.num_tables, w.batch, b.table_row_offset, b.indices,

@@ -29,21 +29,23 @@ def global_rows(w, b):
     return b.table_row_offset[t] + b.indices
 
 
-@pytest.mark.parametrize("bound", ["table-local", "global"])
+@pytest.mark.parametrize("bound,fused", [("table-local", True), ("table-local", False),
+                                         ("global", False)])
 @pytest.mark.parametrize("name", list(SMALL))
-def test_two_steps_match_oracle(name, bound):
+def test_two_steps_match_oracle(name, bound, fused):
     """bound: the cast sorts on table-local rows (the table size is passed as
-    the bound) or on global rows (no bound)."""
+    the bound) or on global rows (no bound). fused: backward and update as
+    one call (tc_embed_backward_update) or as two."""
     w = SMALL[name]
     batches = [wl.make_batch(w, s) for s in (0, 1)]
     touched = np.unique(np.concatenate([global_rows(w, b) for b in batches]))
-    print(f"\n[{name} {bound}] pairs {[b.num_pairs for b in batches]} touched {len(touched)}",
-          flush=True)
+    print(f"\n[{name} {bound} fused={fused}] pairs {[b.num_pairs for b in batches]} "
+          f"touched {len(touched)}", flush=True)
     run = GpuRun(w, max_pairs=max(b.num_pairs for b in batches),
                  max_table_rows=None if bound == "table-local" else 0)
     model = OracleModel(w, touched)
     for b in batches:
-        out, cast, coal = run.step(b)
+        out, cast, coal = run.step(b, fused=fused)
         r_out, r_cast, r_coal, r_rows = model.step(b)
         assert_close(out, r_out, "forward out", bitwise=True)
         compare_cast(cast, r_cast, b.num_pairs)
