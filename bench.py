@@ -77,7 +77,7 @@ def load_traffic(call: str, workload: str):
     return entry["hbm_bytes_per_launch"]
 
 
-def write_traffic(pmc_dir: str, workload: str) -> dict:
+def write_traffic(pmc_dir: str, workload: str, calls) -> dict:
     """Turn four rocprofv3 --pmc CSV runs into HBM bytes per call launch and
     store them in profiles/traffic.json under "<call>:<workload>".
 
@@ -109,7 +109,8 @@ def write_traffic(pmc_dir: str, workload: str) -> dict:
     fetch, write = per_kernel("fetch"), per_kernel("write")
     p = os.path.join(ROOT, "profiles", "traffic.json")
     table = json.load(open(p)) if os.path.exists(p) else {}
-    for call, names in KERNEL_NAMES.items():
+    for call in calls:
+        names = KERNEL_NAMES[call]
         fb = wb = 0.0
         found = True
         for k in names:
@@ -183,7 +184,8 @@ def main():
                          "counter runs in PMC_DIR and exit (no GPU needed)")
     args = ap.parse_args()
     if args.traffic_from:
-        print(json.dumps(write_traffic(args.traffic_from, args.config), indent=1))
+        calls = ["forward", "backward", "update"] if args.unfused else ["forward", "backward_update"]
+        print(json.dumps(write_traffic(args.traffic_from, args.config, calls), indent=1))
         return
     if args.copy_calibration:
         import torch
