@@ -77,6 +77,61 @@ def load_traffic(call: str, workload: str):
     return entry["hbm_bytes_per_launch"]
 
 
+def run_ab(args, w, trainer, dbat, stream):
+    """The paper's backward A/B (Sec. VI-B) on this GPU: baseline gradient
+    expand-coalesce (expand, stable argsort, Algorithm 1 accumulate) against
+    Tensor Casting (cast, Algorithm 3 gather-reduce), same batches, both
+    producing the coalesced gradient rows. Each variant's calls of one step
+    are bracketed by one event pair; the first `warmup` steps are untimed."""
+    import numpy as np
+    import torch
+
+    def variant(name, i):
+        d = dbat[i % NUM_BATCHES]
+        if name == "casted":
+            trainer.cast(d["off"], d["idx"], d["bo"], d["n"], stream)
+            trainer.backward(d["grad"], stream)
+        else:
+            trainer.baseline_backward(d["off"], d["idx"], d["bo"], d["n"], d["grad"], stream)
+
+    times = {"baseline": [], "casted": []}
+    for i in range(args.warmup + args.steps):
+        for name in ("baseline", "casted"):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            variant(name, i)
+            e1.record(stream)
+            if i >= args.warmup:
+                times[name].append((e0, e1))
+    torch.cuda.synchronize()
+    us = {k: float(np.mean([a.elapsed_time(b) for a, b in v])) * 1e3 for k, v in times.items()}
+    uniq = []
+    for i in range(NUM_BATCHES):
+        d = dbat[i]
+        trainer.cast(d["off"], d["idx"], d["bo"], d["n"], stream)
+        uniq.append(int(trainer.num_unique.item()))
+    D4, nb = 4 * w.dim, w.num_bags
+    n = float(np.mean([d["n"] for d in dbat]))
+    u = float(np.mean(uniq))
+    # paper's traffic model (Sec. III-C): expand reads each bag's gradient and
+    # writes N rows; coalesce reads N rows and writes U rows; the casted
+    # gather-reduce reads N (gathered) rows and writes U rows
+    base_bytes = nb * D4 + n * D4 + n * D4 + u * D4 + 3 * n * 4
+    cast_bytes = n * D4 + u * D4 + 2 * n * 4
+    print(json.dumps({
+        "metric": "backward A/B: baseline expand-coalesce vs Tensor Casting, us per step",
+        "config": {"workload": f"{args.config}: {w.name}", "pairs_per_step": round(n, 1),
+                   "unique_rows_per_step": round(u, 1)},
+        "steps": args.steps, "warmup": args.warmup,
+        "baseline_us": round(us["baseline"], 2),
+        "casted_us": round(us["casted"], 2),
+        "speedup": round(us["baseline"] / us["casted"], 3),
+        "algorithmic_bytes": {"baseline": round(base_bytes), "casted": round(cast_bytes),
+                              "ratio": round(base_bytes / cast_bytes, 3)},
+        "note": "both variants include their sort (argsort / cast); dtype f32; data synthetic",
+    }), flush=True)
+
+
 def write_traffic(pmc_dir: str, workload: str, calls) -> dict:
     """Turn four rocprofv3 --pmc CSV runs into HBM bytes per call launch and
     store them in profiles/traffic.json under "<call>:<workload>".
@@ -174,6 +229,9 @@ def main():
     ap.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle work for cpu_baseline (0 disables)")
+    ap.add_argument("--ab", action="store_true",
+                    help="instead of the step: time the paper's baseline backward "
+                         "(expand-coalesce) against the casted backward and exit")
     ap.add_argument("--unfused", action="store_true",
                     help="backward and update as two calls (tc_embed_backward, tc_sparse_update)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -223,6 +281,9 @@ def main():
                  bo=torch.from_numpy(b.bag_offsets).to(dev),
                  grad=torch.from_numpy(b.grad_out).to(dev), n=b.num_pairs) for b in batches]
     stream = torch.cuda.current_stream(dev)
+    if args.ab:
+        run_ab(args, w, trainer, dbat, stream)
+        return
 
     calls = (["forward", "cast", "backward", "update"] if args.unfused
              else ["forward", "cast", "backward_update"])

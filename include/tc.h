@@ -14,6 +14,12 @@
  * tc_embed_backward_update does the last two in one pass (same results bit
  * for bit) without storing the coalesced gradient in device memory.
  *
+ * The paper's baseline backward (gradient expand-coalesce, Sec. II-B and
+ * Algorithm 1), for comparing against the casted one on the same GPU:
+ *   tc_embed_expand    one copy of the output gradient per pair
+ *   tc_argsort_rows    stable argsort of the pairs by row (Algorithm 1's ArgSort)
+ *   tc_embed_coalesce  Algorithm 1's ordered accumulate of the expanded rows
+ *
  * Conventions shared by every call
  * --------------------------------
  * Pointers are DEVICE pointers owned by the caller unless a comment says
@@ -131,6 +137,42 @@ tc_status tc_cast_index(const int64_t *table_row_offset, int32_t num_tables,
                         int32_t *seg_offsets, int32_t *casted_src, int32_t *casted_dst,
                         int32_t *num_unique, void *workspace, size_t workspace_bytes,
                         hipStream_t stream);
+
+/*
+ * Stable argsort of the pairs by row (Algorithm 1's ArgSort, Sec. II-B):
+ * sorted_pos[i] = position j of the i-th pair in row order (equal rows keep
+ * their input order), with unique_rows, seg_offsets and *num_unique as in
+ * tc_cast_index. Arguments, capacities and workspace are those of
+ * tc_cast_index; sorted_pos holds num_pairs entries.
+ */
+tc_status tc_argsort_rows(const int64_t *table_row_offset, int32_t num_tables,
+                          int32_t bags_per_table, int64_t total_rows, int64_t max_table_rows,
+                          const int32_t *indices, const int32_t *bag_offsets, int64_t num_pairs,
+                          int32_t *unique_rows, int32_t *seg_offsets, int32_t *sorted_pos,
+                          int32_t *num_unique, void *workspace, size_t workspace_bytes,
+                          hipStream_t stream);
+
+/*
+ * Gradient expand (Sec. II-B, the baseline backward): for every pair j of
+ * bag g, expanded[j, :] = grad_out[g, :].
+ *   grad_out  [num_bags x dim] fp32; bag_offsets as for tc_cast_index
+ *   expanded  [num_pairs x dim] fp32 (written)
+ */
+tc_status tc_embed_expand(const float *grad_out, int32_t num_bags, int32_t dim,
+                          const int32_t *bag_offsets, int64_t num_pairs, float *expanded,
+                          hipStream_t stream);
+
+/*
+ * Gradient coalescing, Algorithm 1's accumulate: for every u < *num_unique,
+ *   coal_grad[u, :] = sum over i in [seg_offsets[u], seg_offsets[u+1]), in
+ *                     order, of expanded[sorted_pos[i], :], starting from +0,
+ * with seg_offsets and sorted_pos from tc_argsort_rows. Equals
+ * tc_embed_backward's coal_grad bit for bit (same rows, same order).
+ */
+tc_status tc_embed_coalesce(const float *expanded, int64_t num_pairs, int32_t dim,
+                            const int32_t *seg_offsets, const int32_t *sorted_pos,
+                            const int32_t *num_unique, int64_t max_unique, float *coal_grad,
+                            hipStream_t stream);
 
 /*
  * Casted gradient gather-reduce (Algorithm 3): for every u < *num_unique,

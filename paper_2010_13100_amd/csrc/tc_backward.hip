@@ -418,6 +418,63 @@ __global__ __launch_bounds__(kBlock) void k_backward_short(
     }
 }
 
+// Gradient expand (the paper's baseline backward, Sec. II-B): every pair j of
+// bag g gets a copy of grad_out[g]. One lane group per bag holds the row in
+// registers and writes it once per pair of the bag.
+template <int LANES, int CHUNKS>
+__global__ __launch_bounds__(kBlock) void k_expand(const float *__restrict__ grad, int32_t dim,
+                                                  const int32_t *__restrict__ bag_offsets,
+                                                  int64_t num_bags, float *__restrict__ expanded) {
+    constexpr int kGroups = kWave / LANES;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int sub = lane & (LANES - 1);
+    const int grp = lane / LANES;
+    const int d4 = dim >> 2;
+    const int64_t wave = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / kWave;
+    const int64_t nwave = (int64_t(gridDim.x) * blockDim.x) / kWave;
+    for (int64_t g0 = wave * kGroups; g0 < num_bags; g0 += nwave * kGroups) {
+        const int64_t g = g0 + grp;
+        if (g >= num_bags) continue;
+        const int32_t beg = bag_offsets[g], end = bag_offsets[g + 1];
+        float4 v[CHUNKS];
+        const float *row = grad + g * int64_t(dim);
+#pragma unroll
+        for (int c = 0; c < CHUNKS; ++c) {
+            const int col4 = sub + c * LANES;
+            v[c] = col4 < d4 ? *reinterpret_cast<const float4 *>(row + 4 * col4)
+                             : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        for (int32_t j = beg; j < end; ++j)
+            group_store<LANES, CHUNKS>(expanded + int64_t(j) * dim, dim, sub, v);
+    }
+}
+
+tc_status launch_expand(const float *grad, int32_t dim, const int32_t *bag_offsets,
+                        int64_t num_bags, float *expanded, hipStream_t stream) {
+    const RowShape s = row_shape(dim);
+    const int64_t rows_per_block = (kBlock / kWave) * (kWave / s.lanes);
+    const unsigned grid = grid_for(num_bags, rows_per_block, int64_t(kNumCUs) * 8);
+#define TC_EXP_CASE(L, C)                                                                    \
+    if (s.lanes == L && s.chunks == C) {                                                     \
+        k_expand<L, C><<<grid, kBlock, 0, stream>>>(grad, dim, bag_offsets, num_bags,        \
+                                                    expanded);                               \
+        return check_launch("k_expand");                                                     \
+    }
+    TC_EXP_CASE(1, 1)
+    TC_EXP_CASE(2, 1)
+    TC_EXP_CASE(4, 1)
+    TC_EXP_CASE(8, 1)
+    TC_EXP_CASE(16, 1)
+    TC_EXP_CASE(32, 1)
+    TC_EXP_CASE(64, 1)
+    TC_EXP_CASE(64, 2)
+    TC_EXP_CASE(64, 3)
+    TC_EXP_CASE(64, 4)
+#undef TC_EXP_CASE
+    set_error("no expand kernel for dim %d", dim);
+    return TC_ERR_UNSUPPORTED;
+}
+
 tc_status launch_backward(const float *grad, int32_t dim, const int32_t *ids,
                           const int32_t *offsets, const int32_t *num_out_dev, int64_t cap,
                           const RowSink &out, hipStream_t stream) {
@@ -503,5 +560,46 @@ extern "C" tc_status tc_embed_backward_update(
                "tc_embed_backward_update: float pointers must be 16-byte aligned");
     const RowSink sink{coal_grad, W, opt_state, unique_rows, opt_kind, lr, eps};
     return launch_backward(grad_out, dim, casted_src, seg_offsets, num_unique, max_unique, sink,
+                           stream);
+}
+
+extern "C" tc_status tc_embed_expand(const float *grad_out, int32_t num_bags, int32_t dim,
+                                     const int32_t *bag_offsets, int64_t num_pairs,
+                                     float *expanded, hipStream_t stream) {
+    clear_error();
+    TC_REQUIRE(num_bags >= 0 && num_pairs >= 0, TC_ERR_INVALID_ARG,
+               "tc_embed_expand: negative size");
+    TC_REQUIRE(num_pairs < (int64_t(1) << 31), TC_ERR_INVALID_ARG,
+               "tc_embed_expand: num_pairs must be below 2^31");
+    TC_REQUIRE(dim > 0 && dim % 4 == 0 && dim <= kMaxDim, TC_ERR_UNSUPPORTED,
+               "tc_embed_expand: dim %d must be a multiple of 4 in [4, %d]", dim, kMaxDim);
+    if (num_bags == 0 || num_pairs == 0) return TC_OK;
+    TC_REQUIRE(grad_out && bag_offsets && expanded, TC_ERR_INVALID_ARG,
+               "tc_embed_expand: null pointer");
+    TC_REQUIRE(aligned16(grad_out) && aligned16(expanded), TC_ERR_UNSUPPORTED,
+               "tc_embed_expand: grad_out and expanded must be 16-byte aligned");
+    return launch_expand(grad_out, dim, bag_offsets, num_bags, expanded, stream);
+}
+
+extern "C" tc_status tc_embed_coalesce(const float *expanded, int64_t num_pairs, int32_t dim,
+                                       const int32_t *seg_offsets, const int32_t *sorted_pos,
+                                       const int32_t *num_unique, int64_t max_unique,
+                                       float *coal_grad, hipStream_t stream) {
+    clear_error();
+    TC_REQUIRE(num_pairs >= 0 && max_unique >= 0, TC_ERR_INVALID_ARG,
+               "tc_embed_coalesce: negative size");
+    TC_REQUIRE(num_pairs < (int64_t(1) << 31) && max_unique < (int64_t(1) << 31),
+               TC_ERR_INVALID_ARG, "tc_embed_coalesce: sizes must be below 2^31");
+    TC_REQUIRE(dim > 0 && dim % 4 == 0 && dim <= kMaxDim, TC_ERR_UNSUPPORTED,
+               "tc_embed_coalesce: dim %d must be a multiple of 4 in [4, %d]", dim, kMaxDim);
+    if (max_unique == 0) return TC_OK;
+    TC_REQUIRE(expanded && seg_offsets && sorted_pos && num_unique && coal_grad,
+               TC_ERR_INVALID_ARG, "tc_embed_coalesce: null pointer");
+    TC_REQUIRE(aligned16(expanded) && aligned16(coal_grad), TC_ERR_UNSUPPORTED,
+               "tc_embed_coalesce: expanded and coal_grad must be 16-byte aligned");
+    // Algorithm 1's accumulate is the casted gather-reduce over the expanded
+    // rows, in sorted order: the same kernels with sorted positions as ids.
+    const RowSink sink{coal_grad, nullptr, nullptr, nullptr, TC_OPT_SGD, 0.f, 0.f};
+    return launch_backward(expanded, dim, sorted_pos, seg_offsets, num_unique, max_unique, sink,
                            stream);
 }

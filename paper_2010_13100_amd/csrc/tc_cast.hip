@@ -90,13 +90,14 @@ struct alignas(16) TileRec {
 };
 // ---------------------------------------------------------------------------
 // 1. key build: one group of 16 lanes per bag writes that bag's pairs; keys
-// are table-local rows when `local`, else global rows. With `local`, block 0
-// also writes the tile records of the num_tables segments.
+// are table-local rows when `local`, else global rows; values are bag ids
+// (dst), or pair positions when `positions` (an argsort). With `local`, block
+// 0 also writes the tile records of the num_tables segments.
 __global__ __launch_bounds__(kBlock) void k_build_keys(
     const int32_t *__restrict__ indices, const int32_t *__restrict__ bag_offsets,
     const int64_t *__restrict__ table_row_offset, int64_t num_bags, int32_t bags_per_table,
-    int32_t num_tables, bool local, TileRec *__restrict__ tiles, int32_t num_tile_slots,
-    int32_t *__restrict__ keys, int32_t *__restrict__ vals) {
+    int32_t num_tables, bool local, bool positions, TileRec *__restrict__ tiles,
+    int32_t num_tile_slots, int32_t *__restrict__ keys, int32_t *__restrict__ vals) {
     if (local && blockIdx.x == 0) {
         __shared__ int32_t tstart[kMaxSegTables + 1], pstart[kMaxSegTables + 1];
         __shared__ int32_t rowoff[kMaxSegTables];
@@ -150,7 +151,7 @@ __global__ __launch_bounds__(kBlock) void k_build_keys(
         const int64_t base = local ? 0 : table_row_offset[g / bags_per_table];
         for (int32_t j = beg + sub; j < end; j += kLanes) {
             keys[j] = int32_t(base + indices[j]);
-            vals[j] = int32_t(g);
+            vals[j] = positions ? j : int32_t(g);
         }
     }
 }
@@ -574,38 +575,40 @@ extern "C" size_t tc_cast_workspace_bytes(int64_t num_pairs, int64_t total_rows,
     return cast_plan(num_pairs, num_tables).bytes;
 }
 
-extern "C" tc_status tc_cast_index(const int64_t *table_row_offset, int32_t num_tables,
-                                   int32_t bags_per_table, int64_t total_rows,
-                                   int64_t max_table_rows, const int32_t *indices,
-                                   const int32_t *bag_offsets, int64_t num_pairs,
-                                   int32_t *unique_rows, int32_t *seg_offsets,
-                                   int32_t *casted_src, int32_t *casted_dst, int32_t *num_unique,
-                                   void *workspace, size_t workspace_bytes, hipStream_t stream) {
-    clear_error();
+namespace {
+// The sort and segment build behind tc_cast_index (values = bag ids) and
+// tc_argsort_rows (values = pair positions). `what` names the entry point in
+// error messages.
+tc_status cast_impl(const char *what, bool positions, const int64_t *table_row_offset,
+                    int32_t num_tables, int32_t bags_per_table, int64_t total_rows,
+                    int64_t max_table_rows, const int32_t *indices, const int32_t *bag_offsets,
+                    int64_t num_pairs, int32_t *unique_rows, int32_t *seg_offsets,
+                    int32_t *casted_src, int32_t *casted_dst, int32_t *num_unique,
+                    void *workspace, size_t workspace_bytes, hipStream_t stream) {
     TC_REQUIRE(num_tables >= 0 && bags_per_table >= 0 && total_rows >= 0 && num_pairs >= 0 &&
                    max_table_rows >= 0,
-               TC_ERR_INVALID_ARG, "tc_cast_index: negative size");
+               TC_ERR_INVALID_ARG, "%s: negative size", what);
     TC_REQUIRE(total_rows < (int64_t(1) << 31) && num_pairs < (int64_t(1) << 31),
-               TC_ERR_INVALID_ARG, "tc_cast_index: total_rows and num_pairs must be below 2^31");
+               TC_ERR_INVALID_ARG, "%s: total_rows and num_pairs must be below 2^31", what);
     const int64_t num_bags = int64_t(num_tables) * bags_per_table;
     TC_REQUIRE(num_bags < (int64_t(1) << 31), TC_ERR_INVALID_ARG,
-               "tc_cast_index: more than 2^31-1 bags");
-    TC_REQUIRE(seg_offsets && num_unique, TC_ERR_INVALID_ARG, "tc_cast_index: null pointer");
+               "%s: more than 2^31-1 bags", what);
+    TC_REQUIRE(seg_offsets && num_unique, TC_ERR_INVALID_ARG, "%s: null pointer", what);
     if (num_pairs == 0) {
         k_cast_empty<<<1, kWave, 0, stream>>>(seg_offsets, num_unique);
         return check_launch("k_cast_empty");
     }
     TC_REQUIRE(num_bags > 0 && total_rows > 0, TC_ERR_INVALID_ARG,
-               "tc_cast_index: pairs without bags or rows");
+               "%s: pairs without bags or rows", what);
     TC_REQUIRE(table_row_offset && indices && bag_offsets && unique_rows && casted_src,
-               TC_ERR_INVALID_ARG, "tc_cast_index: null pointer");
+               TC_ERR_INVALID_ARG, "%s: null pointer", what);
     const CastPlan plan = cast_plan(num_pairs, num_tables);
     TC_REQUIRE(workspace && workspace_bytes >= plan.bytes, TC_ERR_WORKSPACE,
-               "tc_cast_index: workspace of %zu bytes, %zu needed", workspace_bytes, plan.bytes);
+               "%s: workspace of %zu bytes, %zu needed", what, workspace_bytes, plan.bytes);
     TC_REQUIRE((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) == 0, TC_ERR_WORKSPACE,
-               "tc_cast_index: workspace must be 256-byte aligned");
+               "%s: workspace must be 256-byte aligned", what);
     TC_REQUIRE(plan.sort_tiles < (int64_t(1) << 31) / kMaxRadix, TC_ERR_INVALID_ARG,
-               "tc_cast_index: too many pairs");
+               "%s: too many pairs", what);
 
     // Table-local keys when the tables are known to be small enough to save
     // key bits; otherwise one segment of global rows.
@@ -630,7 +633,7 @@ extern "C" tc_status tc_cast_index(const int64_t *table_row_offset, int32_t num_
         const unsigned grid = grid_for(num_bags, kBlock / 16, int64_t(kNumCUs) * 8);
         k_build_keys<<<grid, kBlock, 0, stream>>>(indices, bag_offsets, table_row_offset,
                                                   num_bags, bags_per_table, num_tables, local,
-                                                  recs, sort_tiles, ka, va);
+                                                  positions, recs, sort_tiles, ka, va);
         tc_status st = check_launch("k_build_keys");
         if (st != TC_OK) return st;
     }
@@ -664,4 +667,33 @@ extern "C" tc_status tc_cast_index(const int64_t *table_row_offset, int32_t num_
     k_seg_write<<<seg_tiles, kBlock, 0, stream>>>(sorted_keys, num_pairs, heads, unique_rows,
                                                   seg_offsets, casted_dst);
     return check_launch("k_seg_write");
+}
+}  // namespace
+
+extern "C" tc_status tc_cast_index(const int64_t *table_row_offset, int32_t num_tables,
+                                   int32_t bags_per_table, int64_t total_rows,
+                                   int64_t max_table_rows, const int32_t *indices,
+                                   const int32_t *bag_offsets, int64_t num_pairs,
+                                   int32_t *unique_rows, int32_t *seg_offsets,
+                                   int32_t *casted_src, int32_t *casted_dst, int32_t *num_unique,
+                                   void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    clear_error();
+    return cast_impl("tc_cast_index", false, table_row_offset, num_tables, bags_per_table,
+                     total_rows, max_table_rows, indices, bag_offsets, num_pairs, unique_rows,
+                     seg_offsets, casted_src, casted_dst, num_unique, workspace,
+                     workspace_bytes, stream);
+}
+
+extern "C" tc_status tc_argsort_rows(const int64_t *table_row_offset, int32_t num_tables,
+                                     int32_t bags_per_table, int64_t total_rows,
+                                     int64_t max_table_rows, const int32_t *indices,
+                                     const int32_t *bag_offsets, int64_t num_pairs,
+                                     int32_t *unique_rows, int32_t *seg_offsets,
+                                     int32_t *sorted_pos, int32_t *num_unique, void *workspace,
+                                     size_t workspace_bytes, hipStream_t stream) {
+    clear_error();
+    return cast_impl("tc_argsort_rows", true, table_row_offset, num_tables, bags_per_table,
+                     total_rows, max_table_rows, indices, bag_offsets, num_pairs, unique_rows,
+                     seg_offsets, sorted_pos, nullptr, num_unique, workspace, workspace_bytes,
+                     stream);
 }

@@ -31,6 +31,10 @@ _SIGNATURES = {
                                 _vp]),
     "tc_embed_backward_update": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _vp,
                                         _i64, _i32, _f32, _f32, _vp, _vp]),
+    "tc_argsort_rows": (_i32, [_vp, _i32, _i32, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp,
+                               _vp, _sz, _vp]),
+    "tc_embed_expand": (_i32, [_vp, _i32, _i32, _vp, _i64, _vp, _vp]),
+    "tc_embed_coalesce": (_i32, [_vp, _i64, _i32, _vp, _vp, _vp, _i64, _vp, _vp]),
     "tc_status_string": (ctypes.c_char_p, [_i32]),
     "tc_last_error": (ctypes.c_char_p, []),
     "tc_abi_version": (_i32, []),
@@ -143,6 +147,36 @@ def tc_embed_backward_update(grad_out, seg_offsets, casted_src, unique_rows, num
         _stream(stream)), "tc_embed_backward_update")
 
 
+def tc_argsort_rows(table_row_offset, num_tables, bags_per_table, total_rows, max_table_rows,
+                    indices, bag_offsets, num_pairs, unique_rows, seg_offsets, sorted_pos,
+                    num_unique, workspace, stream=None) -> None:
+    _check(_lib.tc_argsort_rows(
+        _ptr(table_row_offset, torch.int64, "table_row_offset"), num_tables, bags_per_table,
+        total_rows, max_table_rows, _ptr(indices, torch.int32, "indices"),
+        _ptr(bag_offsets, torch.int32, "bag_offsets"), num_pairs,
+        _ptr(unique_rows, torch.int32, "unique_rows"), _ptr(seg_offsets, torch.int32, "seg_offsets"),
+        _ptr(sorted_pos, torch.int32, "sorted_pos"), _ptr(num_unique, torch.int32, "num_unique"),
+        _ptr(workspace, None, "workspace"),
+        0 if workspace is None else workspace.numel() * workspace.element_size(),
+        _stream(stream)), "tc_argsort_rows")
+
+
+def tc_embed_expand(grad_out, bag_offsets, num_pairs, expanded, stream=None) -> None:
+    _check(_lib.tc_embed_expand(
+        _ptr(grad_out, torch.float32, "grad_out"), grad_out.shape[0], grad_out.shape[1],
+        _ptr(bag_offsets, torch.int32, "bag_offsets"), num_pairs,
+        _ptr(expanded, torch.float32, "expanded"), _stream(stream)), "tc_embed_expand")
+
+
+def tc_embed_coalesce(expanded, num_pairs, seg_offsets, sorted_pos, num_unique, max_unique,
+                      coal_grad, stream=None) -> None:
+    _check(_lib.tc_embed_coalesce(
+        _ptr(expanded, torch.float32, "expanded"), num_pairs, expanded.shape[1],
+        _ptr(seg_offsets, torch.int32, "seg_offsets"), _ptr(sorted_pos, torch.int32, "sorted_pos"),
+        _ptr(num_unique, torch.int32, "num_unique"), max_unique,
+        _ptr(coal_grad, torch.float32, "coal_grad"), _stream(stream)), "tc_embed_coalesce")
+
+
 class EmbeddingTrainer:
     """Device buffers for one workload shape and the four calls of a step.
 
@@ -193,6 +227,23 @@ class EmbeddingTrainer:
     def update(self, stream=None):
         tc_sparse_update(self.W, self.A, self.unique_rows, self.coal, self.num_unique,
                          self.max_unique, self.opt_kind, self.lr, self.eps, stream)
+
+    def baseline_backward(self, table_row_offset, indices, bag_offsets, num_pairs, grad_out,
+                          stream=None):
+        """The paper's baseline backward (expand, stable argsort, Algorithm 1
+        accumulate) into self.coal, with the same unique_rows / seg_offsets as
+        the cast; needs self.expanded ([max_pairs x dim], allocated here on
+        first use) and overwrites casted_src with the sorted positions."""
+        if getattr(self, "expanded", None) is None:
+            self.expanded = torch.empty((max(self.max_pairs, 1), self.dim), dtype=torch.float32,
+                                        device=self.W.device)
+        tc_embed_expand(grad_out, bag_offsets, num_pairs, self.expanded, stream)
+        tc_argsort_rows(table_row_offset, self.num_tables, self.bags_per_table, self.total_rows,
+                        self.max_table_rows, indices, bag_offsets, num_pairs, self.unique_rows,
+                        self.seg_offsets, self.casted_src, self.num_unique, self.workspace,
+                        stream)
+        tc_embed_coalesce(self.expanded, num_pairs, self.seg_offsets, self.casted_src,
+                          self.num_unique, self.max_unique, self.coal, stream)
 
     def backward_update(self, grad_out, stream=None, store_coal=False):
         """backward + update in one pass (coal stored only if store_coal)."""

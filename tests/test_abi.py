@@ -128,6 +128,10 @@ def test_cast_rejects_bad_arguments(tc):
     assert f(ur=None) == tc.TC_ERR_INVALID_ARG
     assert f(nu=None) == tc.TC_ERR_INVALID_ARG
     assert f(T=0) == tc.TC_ERR_INVALID_ARG     # pairs but no bags
+    # the argsort shares the cast's checks, under its own name
+    rc = lib.tc_argsort_rows(h.lp(), 1, 50, 100, 100, h.ip(), h.ip(), 1000, h.ip(), h.ip(),
+                             h.ip(), h.ip(), h.wsp(), need - 1, None)
+    assert rc == tc.TC_ERR_WORKSPACE and "tc_argsort_rows" in _err(tc)
     assert h.untouched()
 
 
@@ -173,6 +177,24 @@ def test_backward_and_update_reject_bad_arguments(tc):
     assert fused(coal=h.fp(misalign=True)) == tc.TC_ERR_UNSUPPORTED
     assert fused(W=h.fp(misalign=True)) == tc.TC_ERR_UNSUPPORTED
     assert fused(mu=0) == tc.TC_OK
+
+    def expand(**k):
+        return lib.tc_embed_expand(k.get("g", h.fp()), k.get("nb", 10), k.get("dim", 8),
+                                   k.get("bo", h.ip()), k.get("n", 10), k.get("e", h.fp()), None)
+    assert expand(dim=2) == tc.TC_ERR_UNSUPPORTED
+    assert expand(n=-1) == tc.TC_ERR_INVALID_ARG
+    assert expand(e=None) == tc.TC_ERR_INVALID_ARG
+    assert expand(e=h.fp(misalign=True)) == tc.TC_ERR_UNSUPPORTED
+    assert expand(n=0) == tc.TC_OK
+
+    def coalesce(**k):
+        return lib.tc_embed_coalesce(k.get("e", h.fp()), k.get("n", 10), k.get("dim", 8),
+                                     k.get("so", h.ip()), k.get("sp", h.ip()), k.get("nu", h.ip()),
+                                     k.get("mu", 10), k.get("coal", h.fp()), None)
+    assert coalesce(dim=1030) == tc.TC_ERR_UNSUPPORTED
+    assert coalesce(mu=-3) == tc.TC_ERR_INVALID_ARG
+    assert coalesce(sp=None) == tc.TC_ERR_INVALID_ARG
+    assert coalesce(mu=0) == tc.TC_OK
     assert h.untouched()
 
 
