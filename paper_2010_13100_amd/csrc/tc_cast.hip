@@ -185,6 +185,20 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool ok) {
     return peers;
 }
 
+// The same with the digit width known only at run time (uniform branches).
+__device__ __forceinline__ uint64_t match_digit_n(uint32_t d, bool ok, int bits) {
+    uint64_t peers = __ballot(ok);
+#pragma unroll
+    for (int b = 0; b < kMaxRadixBits; ++b) {
+        if (b < bits) {
+            const bool bit = (d >> b) & 1u;
+            const uint64_t m = __ballot(bit);
+            peers &= bit ? m : ~m;
+        }
+    }
+    return peers;
+}
+
 // ---------------------------------------------------------------------------
 // 2a. per-tile digit histogram -> counts[digit * tiles + tile]. Equal digits
 // within a wavefront are counted by one lane (no LDS atomic conflicts under
@@ -483,6 +497,177 @@ __global__ __launch_bounds__(kBlock) void k_seg_write(
     }
 }
 
+// ---------------------------------------------------------------------------
+// Small batches (at most kSmallPairs pairs): the whole cast in one workgroup
+// of kSmallThreads threads, keys and values in LDS. Same stable LSD passes
+// (wave w owns positions [w*kSmallSpan, (w+1)*kSmallSpan), walked 64 at a
+// time; equal digits ranked with ballots and one LDS atomic per digit group)
+// and the same segment build, without the kernel chain: for a few thousand
+// pairs the multi-kernel cast is all launch and memory latency.
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallWaves = kSmallThreads / kWave;  // 16
+constexpr int kSmallItems = 8;
+constexpr int kSmallSpan = kWave * kSmallItems;     // 512
+constexpr int kSmallPairs = kSmallWaves * kSmallSpan;  // 8192
+
+// Block-wide exclusive scan over the kSmallThreads threads.
+__device__ __forceinline__ int32_t small_block_scan(int32_t v, int32_t *total) {
+    __shared__ int32_t wsum[kSmallWaves];
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+    int32_t incl = v;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int32_t o = __shfl_up(incl, off, kWave);
+        if (lane >= off) incl += o;
+    }
+    if (lane == kWave - 1) wsum[w] = incl;
+    __syncthreads();
+    int32_t wbase = 0, tot = 0;
+#pragma unroll
+    for (int ww = 0; ww < kSmallWaves; ++ww) {
+        const int32_t s = wsum[ww];
+        if (ww < w) wbase += s;
+        tot += s;
+    }
+    __syncthreads();
+    *total = tot;
+    return wbase + incl - v;
+}
+
+__global__ __launch_bounds__(kSmallThreads) void k_cast_small(
+    const int32_t *__restrict__ indices, const int32_t *__restrict__ bag_offsets,
+    const int64_t *__restrict__ table_row_offset, int32_t num_tables, int32_t num_bags,
+    int32_t bags_per_table, int32_t n, int bits, bool positions, int32_t *__restrict__ unique_rows,
+    int32_t *__restrict__ seg_offsets, int32_t *__restrict__ casted_src,
+    int32_t *__restrict__ casted_dst, int32_t *__restrict__ num_unique) {
+    __shared__ int32_t keys[2][kSmallPairs];
+    __shared__ int32_t vals[2][kSmallPairs];
+    __shared__ int32_t wcount[kSmallWaves][kMaxRadix];
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+
+    // (src, dst) pairs from the bag-major CSR index: 16 lanes per bag. The
+    // index, the bag offsets and the table offsets are first staged in LDS
+    // (in the second key and value buffers and the digit counters) with
+    // independent loads, so the walk over bags waits for memory once.
+    {
+        constexpr int kLanes = 16;
+        const int sub = tid & (kLanes - 1);
+        const bool staged = num_bags < kSmallPairs && num_tables <= kSmallWaves * kMaxRadix;
+        int32_t *s_idx = keys[1], *s_bo = vals[1], *s_off = &wcount[0][0];
+        if (staged) {
+            for (int32_t j = tid; j < n; j += kSmallThreads) s_idx[j] = indices[j];
+            for (int32_t g = tid; g <= num_bags; g += kSmallThreads) s_bo[g] = bag_offsets[g];
+            for (int32_t t = tid; t < num_tables; t += kSmallThreads)
+                s_off[t] = int32_t(table_row_offset[t]);
+            __syncthreads();
+        }
+        for (int32_t g = tid / kLanes; g < num_bags; g += kSmallThreads / kLanes) {
+            const int32_t beg = staged ? s_bo[g] : bag_offsets[g];
+            const int32_t end = staged ? s_bo[g + 1] : bag_offsets[g + 1];
+            const int32_t t = g / bags_per_table;
+            const int32_t base = staged ? s_off[t] : int32_t(table_row_offset[t]);
+            for (int32_t j = beg + sub; j < end; j += kLanes) {
+                keys[0][j] = base + (staged ? s_idx[j] : indices[j]);
+                vals[0][j] = positions ? j : g;
+            }
+        }
+    }
+    __syncthreads();
+
+    const int passes = (bits + kMaxRadixBits - 1) / kMaxRadixBits;
+    const int per_pass = (bits + passes - 1) / passes;
+    const int32_t base = w * kSmallSpan;
+    int cur = 0;
+    for (int p = 0; p < passes; ++p) {
+        const int shift = p * per_pass;
+        const int pbits = shift + per_pass <= bits ? per_pass : bits - shift;
+        const uint32_t mask = (1u << pbits) - 1u;
+        for (int i = tid; i < kSmallWaves * kMaxRadix; i += kSmallThreads)
+            (&wcount[0][0])[i] = 0;
+        __syncthreads();
+        int32_t key[kSmallItems], val[kSmallItems], lower_n[kSmallItems], leader[kSmallItems],
+            old[kSmallItems];
+#pragma unroll
+        for (int i = 0; i < kSmallItems; ++i) {
+            const int32_t j = base + i * kWave + lane;
+            const bool ok = j < n;
+            key[i] = ok ? keys[cur][j] : 0;
+            val[i] = ok ? vals[cur][j] : 0;
+            const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
+            const uint64_t peers = match_digit_n(d, ok, pbits);
+            const uint64_t lower = peers & lanemask_lt(lane);
+            lower_n[i] = __popcll(lower);
+            leader[i] = peers ? __builtin_ctzll(peers) : lane;
+            old[i] = 0;
+            if (ok && lower == 0) old[i] = atomicAdd(&wcount[w][d], __popcll(peers));
+        }
+        int32_t rank[kSmallItems];
+#pragma unroll
+        for (int i = 0; i < kSmallItems; ++i)
+            rank[i] = __shfl(old[i], leader[i], kWave) + lower_n[i];
+        __syncthreads();
+        {
+            // digit d = tid (threads past the radix hold zeros): start of each
+            // wave's run, in digit order then wave order
+            int32_t c[kSmallWaves], my = 0;
+#pragma unroll
+            for (int ww = 0; ww < kSmallWaves; ++ww) {
+                c[ww] = tid < kMaxRadix ? wcount[ww][tid] : 0;
+                my += c[ww];
+            }
+            int32_t tot;
+            int32_t r = small_block_scan(my, &tot);
+            if (tid < kMaxRadix) {
+#pragma unroll
+                for (int ww = 0; ww < kSmallWaves; ++ww) {
+                    wcount[ww][tid] = r;
+                    r += c[ww];
+                }
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < kSmallItems; ++i) {
+            if (base + i * kWave + lane < n) {
+                const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
+                const int32_t lp = wcount[w][d] + rank[i];
+                keys[cur ^ 1][lp] = key[i];
+                vals[cur ^ 1][lp] = val[i];
+            }
+        }
+        __syncthreads();
+        cur ^= 1;
+    }
+
+    // segment build: thread tid owns sorted positions tid*8 .. tid*8+7
+    int32_t head[kSmallItems], c = 0;
+#pragma unroll
+    for (int i = 0; i < kSmallItems; ++i) {
+        const int32_t j = tid * kSmallItems + i;
+        head[i] = j < n && (j == 0 || keys[cur][j] != keys[cur][j - 1]);
+        c += head[i];
+    }
+    int32_t total;
+    int32_t run = small_block_scan(c, &total);
+#pragma unroll
+    for (int i = 0; i < kSmallItems; ++i) {
+        const int32_t j = tid * kSmallItems + i;
+        if (j < n) {
+            run += head[i];
+            casted_src[j] = vals[cur][j];
+            if (casted_dst) casted_dst[j] = run - 1;
+            if (head[i]) {
+                unique_rows[run - 1] = keys[cur][j];
+                seg_offsets[run - 1] = j;
+            }
+        }
+    }
+    if (tid == 0) {
+        seg_offsets[total] = n;
+        *num_unique = total;
+    }
+}
+
 // No pairs: zero segments, seg_offsets[0] = 0.
 __global__ void k_cast_empty(int32_t *seg_offsets, int32_t *num_unique) {
     if (threadIdx.x == 0) {
@@ -610,6 +795,14 @@ tc_status cast_impl(const char *what, bool positions, const int64_t *table_row_o
     TC_REQUIRE(plan.sort_tiles < (int64_t(1) << 31) / kMaxRadix, TC_ERR_INVALID_ARG,
                "%s: too many pairs", what);
 
+    if (num_pairs <= kSmallPairs) {
+        // one workgroup in LDS (the workspace is not touched)
+        k_cast_small<<<1, kSmallThreads, 0, stream>>>(
+            indices, bag_offsets, table_row_offset, num_tables, int32_t(num_bags), bags_per_table,
+            int32_t(num_pairs), key_bits(total_rows), positions, unique_rows, seg_offsets,
+            casted_src, casted_dst, num_unique);
+        return check_launch("k_cast_small");
+    }
     // Table-local keys when the tables are known to be small enough to save
     // key bits; otherwise one segment of global rows.
     const int global_bits = key_bits(total_rows);

@@ -116,3 +116,10 @@ def test_bound_variants_agree():
 def test_single_table_and_keys_of_one_bit():
     check("one table", [2], [9000], bags_per_table=11, seed=9)
     check("rows of one", [1, 1, 1], [3000, 1, 2049], bags_per_table=2, seed=11)
+
+
+def test_single_workgroup_cast_boundary():
+    # up to 8192 pairs the cast runs in one workgroup; one pair more takes
+    # the multi-kernel sort
+    for n in (8191, 8192, 8193):
+        check(f"n={n}", [3000, 500], [n - 600, 600], bags_per_table=9, seed=n)
