@@ -87,6 +87,10 @@ class Oracle:
             "oracle_casted_gather_reduce": (ctypes.c_int, [i32, i64, vp, vp, vp, i64, i64, vp]),
             "oracle_scatter_sgd": (ctypes.c_int, [i32, i64, vp, vp, dbl, vp, i64, vp]),
             "oracle_scatter_adagrad": (ctypes.c_int, [i32, i64, vp, vp, dbl, dbl, vp, i64, vp, vp]),
+            "oracle_scatter_rmsprop": (ctypes.c_int,
+                                       [i32, i64, vp, vp, dbl, dbl, dbl, vp, i64, vp, vp]),
+            "oracle_scatter_rowwise_adagrad": (ctypes.c_int,
+                                               [i32, i64, vp, vp, dbl, dbl, vp, i64, vp, vp]),
         }
         for name, (res, args) in sig.items():
             f = getattr(lib, name)
@@ -188,6 +192,30 @@ class Oracle:
                                                float(lr), float(eps), _ptr(ids), table.shape[0],
                                                _ptr(table), _ptr(acc)), "scatter_adagrad")
 
+    def scatter_rmsprop(self, rows, coal, lr, eps, gamma, table, acc, table_ids=None):
+        """Eq. (1); updates ``table`` and ``acc`` (same row set) in place."""
+        assert table.dtype == self.dtype and acc.dtype == self.dtype
+        assert table.shape == acc.shape and table.flags.c_contiguous and acc.flags.c_contiguous
+        c = self._real(coal)
+        ids = None if table_ids is None else np.ascontiguousarray(table_ids, dtype=np.int64)
+        _check(self.lib.oracle_scatter_rmsprop(table.shape[1], len(rows),
+                                               _ptr(np.ascontiguousarray(rows, np.int64)), _ptr(c),
+                                               float(lr), float(eps), float(gamma), _ptr(ids),
+                                               table.shape[0], _ptr(table), _ptr(acc)),
+               "scatter_rmsprop")
+
+    def scatter_rowwise_adagrad(self, rows, coal, lr, eps, table, acc, table_ids=None):
+        """Row-wise Adagrad; ``acc`` has one value per stored table row."""
+        assert table.dtype == self.dtype and acc.dtype == self.dtype
+        assert acc.shape == (table.shape[0],) and table.flags.c_contiguous
+        assert acc.flags.c_contiguous
+        c = self._real(coal)
+        ids = None if table_ids is None else np.ascontiguousarray(table_ids, dtype=np.int64)
+        _check(self.lib.oracle_scatter_rowwise_adagrad(
+            table.shape[1], len(rows), _ptr(np.ascontiguousarray(rows, np.int64)), _ptr(c),
+            float(lr), float(eps), _ptr(ids), table.shape[0], _ptr(table), _ptr(acc)),
+            "scatter_rowwise_adagrad")
+
 
 @dataclass
 class StepResult:
@@ -201,7 +229,7 @@ class StepResult:
 
 def train_step(orc: Oracle, *, num_tables, bags_per_table, table_row_offset, indices, bag_offsets,
                grad_out, table, table_ids=None, optimizer="sgd", lr=0.01, eps=1e-8, acc=None,
-               timings: dict | None = None) -> StepResult:
+               gamma=0.99, timings: dict | None = None) -> StepResult:
     """One oracle training step: forward, the paper's baseline backward
     (expand, then Algorithm 1), Tensor Casting (Algorithm 2) for the index
     outputs, and the scatter update. ``table``/``acc`` are copied, not
@@ -233,6 +261,13 @@ def train_step(orc: Oracle, *, num_tables, bags_per_table, table_row_offset, ind
     elif optimizer == "adagrad":
         new_acc = (np.zeros_like(tbl) if acc is None else np.array(acc, dtype=orc.dtype, copy=True))
         orc.scatter_adagrad(rows, coal, lr, eps, tbl, new_acc, table_ids)
+    elif optimizer == "rmsprop":
+        new_acc = (np.zeros_like(tbl) if acc is None else np.array(acc, dtype=orc.dtype, copy=True))
+        orc.scatter_rmsprop(rows, coal, lr, eps, gamma, tbl, new_acc, table_ids)
+    elif optimizer == "rowwise_adagrad":
+        new_acc = (np.zeros(tbl.shape[0], orc.dtype) if acc is None
+                   else np.array(acc, dtype=orc.dtype, copy=True))
+        orc.scatter_rowwise_adagrad(rows, coal, lr, eps, tbl, new_acc, table_ids)
     else:
         raise ValueError(optimizer)
     tick("update", t0)

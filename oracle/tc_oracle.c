@@ -18,6 +18,10 @@
  *   oracle_casted_gather_reduce    casted gradient gather-reduce, Algorithm 3
  *   oracle_scatter_sgd             gradient scatter with plain SGD, Sec. II-B
  *   oracle_scatter_adagrad         gradient scatter with Adagrad, Eq. (2)
+ *   oracle_scatter_rmsprop         gradient scatter with RMSprop, Eq. (1)
+ *   oracle_scatter_rowwise_adagrad gradient scatter with row-wise Adagrad, a
+ *                                  variant of Eq. (2) that the paper does
+ *                                  not define (one accumulator per row)
  *
  * The arithmetic type is fixed at build time: -DOREAL=double gives the
  * reference used to pin the method against closed forms, -DOREAL=float
@@ -34,7 +38,12 @@
  *  - the reduction is a sum; sums run sequentially in index order;
  *  - Algorithm 3's coalesced-gradient array starts at zero;
  *  - Adagrad's accumulator starts at zero and epsilon sits inside the square
- *    root, as Eq. (2) writes it.
+ *    root, as Eq. (2) writes it;
+ *  - RMSprop's decay gamma is a parameter (the paper gives no value), and
+ *    its update is lazy like the others: rows without a gradient in the
+ *    step keep W and A, their A is not decayed;
+ *  - row-wise Adagrad adds the mean of the row's squared gradient to the
+ *    row's accumulator and divides every element by the one square root.
  *
  * Tables are passed as a row set: `ids` is either NULL (dense table, row r
  * stored at r*dim) or a strictly increasing list of the global row ids that
@@ -368,6 +377,84 @@ int oracle_scatter_adagrad(int32_t dim, int64_t num_unique, const int64_t *rows,
             real sq = g[d] * g[d];
             a[d] = a[d] + sq;
             real s = real_sqrt(reps + a[d]);
+            real q = g[d] / s;
+            real step = rlr * q;
+            w[d] = w[d] - step;
+        }
+    }
+    return 0;
+}
+
+/*
+ * Gradient scatter with RMSprop, Eq. (1): the accumulator becomes a running
+ * average of squared gradients, A <- gamma*A + (1-gamma)*G^2, and then
+ * W <- W - lr * G / sqrt(eps + A), element by element, for the rows that
+ * have a coalesced gradient. Rows without a gradient keep W and A (the same
+ * lazy update as the Adagrad scatter). Order of operations:
+ * t = gamma*A; c = 1 - gamma; A = t + c*(G*G); s = sqrt(eps + A);
+ * q = G / s; W = W - lr * q.
+ */
+int oracle_scatter_rmsprop(int32_t dim, int64_t num_unique, const int64_t *rows,
+                           const real *coal, double lr, double eps, double gamma,
+                           const int64_t *tbl_ids, int64_t tbl_rows, real *tbl, real *acc)
+{
+    if (dim <= 0 || num_unique < 0)
+        return ORACLE_ERR_ARG;
+    const real rlr = (real)lr, reps = (real)eps, rg = (real)gamma;
+    const real rc = (real)1 - rg;
+    for (int64_t u = 0; u < num_unique; ++u) {
+        real *w = row_at(tbl, tbl_ids, tbl_rows, dim, rows[u]);
+        real *a = row_at(acc, tbl_ids, tbl_rows, dim, rows[u]);
+        if (w == NULL || a == NULL)
+            return ORACLE_ERR_ROW;
+        const real *g = coal + u * dim;
+        for (int32_t d = 0; d < dim; ++d) {
+            real t = rg * a[d];
+            real sq = g[d] * g[d];
+            real m = rc * sq;
+            a[d] = t + m;
+            real s = real_sqrt(reps + a[d]);
+            real q = g[d] / s;
+            real step = rlr * q;
+            w[d] = w[d] - step;
+        }
+    }
+    return 0;
+}
+
+/*
+ * Gradient scatter with row-wise Adagrad: Eq. (2) with one accumulator per
+ * embedding row instead of one per element, the accumulator growing by the
+ * mean of the row's squared gradient. For each row with a coalesced
+ * gradient G (dim elements):
+ * m = (G_0^2 + G_1^2 + ... + G_{dim-1}^2) / dim, summed in column order
+ * from zero; A = A + m; s = sqrt(eps + A); then for every d:
+ * q = G_d / s; W_d = W_d - lr * q.
+ * `acc` holds one value per row, stored with the same row set as the table.
+ */
+int oracle_scatter_rowwise_adagrad(int32_t dim, int64_t num_unique, const int64_t *rows,
+                                   const real *coal, double lr, double eps,
+                                   const int64_t *tbl_ids, int64_t tbl_rows, real *tbl,
+                                   real *acc)
+{
+    if (dim <= 0 || num_unique < 0)
+        return ORACLE_ERR_ARG;
+    const real rlr = (real)lr, reps = (real)eps, rdim = (real)dim;
+    for (int64_t u = 0; u < num_unique; ++u) {
+        real *w = row_at(tbl, tbl_ids, tbl_rows, dim, rows[u]);
+        real *a = row_at(acc, tbl_ids, tbl_rows, 1, rows[u]);
+        if (w == NULL || a == NULL)
+            return ORACLE_ERR_ROW;
+        const real *g = coal + u * dim;
+        real ss = 0;
+        for (int32_t d = 0; d < dim; ++d) {
+            real sq = g[d] * g[d];
+            ss = ss + sq;
+        }
+        real m = ss / rdim;
+        a[0] = a[0] + m;
+        real s = real_sqrt(reps + a[0]);
+        for (int32_t d = 0; d < dim; ++d) {
             real q = g[d] / s;
             real step = rlr * q;
             w[d] = w[d] - step;

@@ -274,6 +274,111 @@ def pin_adagrad_closed_form(orc):
     assert np.allclose(t, t2, rtol=tol, atol=tol)
 
 
+
+def pin_rmsprop_special_cases(orc):
+    """Eq. (1) at its two ends and at a dyadic middle point, all exact:
+    gamma = 0 forgets the past (A = G^2), so one step equals Adagrad's first
+    step from A = 0; gamma = 1 keeps A, so W moves by lr*G/sqrt(eps + A0);
+    gamma = 0.75 with A0 = 4, G = 2 gives A = 3 + 1 = 4 (a fixed point)."""
+    lr = 0.5
+    tbl = np.array([[1.0, 2.0, -3.0, 0.0], [4.0, 5.0, 6.0, 7.0], [8.0, 8.5, 9.0, 9.5]])
+    rows = np.array([0, 2])
+    coal = np.array([[0.75, -0.75, 0.0, 0.75], [-0.75, 0.75, 0.75, -0.75]])
+    # gamma = 0 against the Adagrad routine, from a non-zero A0 it must ignore
+    eps = 0.4375
+    t_r, a_r = tbl.astype(orc.dtype).copy(), np.full(tbl.shape, 9.0, orc.dtype)
+    orc.scatter_rmsprop(rows, coal, lr, eps, 0.0, t_r, a_r)
+    t_a, a_a = tbl.astype(orc.dtype).copy(), np.zeros(tbl.shape, orc.dtype)
+    orc.scatter_adagrad(rows, coal, lr, eps, t_a, a_a)
+    a_a[1] = 9.0                            # the untouched row keeps its A
+    assert np.array_equal(t_r, t_a) and np.array_equal(a_r, a_a)
+    want = tbl.copy()
+    want[rows] -= lr * coal                 # eps + G^2 = 1
+    assert np.array_equal(t_r, want)
+    # gamma = 1: A unchanged (eps + A0 = 4), W -= lr * G / 2
+    eps = 1.75
+    a0 = np.full(tbl.shape, 2.25)
+    t, a = tbl.astype(orc.dtype).copy(), a0.astype(orc.dtype).copy()
+    orc.scatter_rmsprop(rows, coal, lr, eps, 1.0, t, a)
+    want = tbl.copy()
+    want[rows] -= lr * coal / 2
+    assert np.array_equal(t, want) and np.array_equal(a, a0)
+    # gamma = 0.75, A0 = 4, |G| = 2: A stays 4; eps = 5 -> sqrt(9) = 3
+    g2 = np.array([[2.0, -2.0, 2.0, -2.0], [-2.0, 2.0, 2.0, 2.0]])
+    a0 = np.full(tbl.shape, 4.0)
+    a0[1] = 1.0
+    t, a = tbl.astype(orc.dtype).copy(), a0.astype(orc.dtype).copy()
+    orc.scatter_rmsprop(rows, g2, 0.75, 5.0, 0.75, t, a)
+    want = tbl.copy()
+    want[rows] -= 0.75 * g2 / 3             # 0.75 * (+-2/3) = +-0.5 up to rounding
+    assert np.array_equal(a, a0)
+    tol = 6e-7 if orc.dtype == np.float32 else 2e-15
+    assert np.allclose(t, want, rtol=0, atol=tol)
+
+
+def pin_rmsprop_geometric(orc):
+    """k steps of Eq. (1) from A = 0 with a constant gradient G give the
+    geometric-series closed form A_k = (1 - gamma^k) G^2, and W moves by
+    lr * G * sum_i 1 / sqrt(eps + A_i). gamma = 0.9 is not symmetric, so a
+    swap of gamma and 1 - gamma gives (1 - 0.1^k) G^2 instead."""
+    gamma, lr, eps, k = 0.9, 0.01, 1e-3, 6
+    G = np.array([[0.5, -1.25, 3.0], [2.0, 0.0, -0.125]])
+    rows = np.array([1, 3])
+    tbl = np.arange(15, dtype=np.float64).reshape(5, 3) * 0.25
+    t, a = tbl.astype(orc.dtype).copy(), np.zeros(tbl.shape, orc.dtype)
+    want_t = tbl.copy()
+    for i in range(1, k + 1):
+        orc.scatter_rmsprop(rows, G, lr, eps, gamma, t, a)
+        a_i = (1 - gamma ** i) * G ** 2
+        want_t[rows] -= lr * G / np.sqrt(eps + a_i)
+    tol = 5e-6 if orc.dtype == np.float32 else 1e-13
+    assert np.allclose(a[rows], (1 - gamma ** k) * G ** 2, rtol=tol, atol=tol)
+    assert np.allclose(t, want_t, rtol=tol, atol=tol)
+    untouched = np.setdiff1d(np.arange(5), rows)
+    assert np.array_equal(t[untouched], tbl[untouched].astype(orc.dtype))
+    assert not np.any(a[untouched])
+
+
+def pin_rowwise_adagrad_special_cases(orc):
+    """Row-wise Adagrad: with dim = 1 it is elementwise Adagrad (the Adagrad
+    routine, bit for bit, over two steps); when every column of a row has the
+    same |G| the row mean is G^2 and it is elementwise Adagrad again; and
+    G = (2, 0, 0, 0) has mean 1, so with eps = 3 the step is G / 2 exactly."""
+    lr, eps = 0.5, 0.4375
+    rows = np.array([0, 2, 3])
+    # dim = 1
+    tbl = np.array([[1.0], [2.0], [-3.0], [0.5]])
+    t_r, a_r = tbl.astype(orc.dtype).copy(), np.zeros(4, orc.dtype)
+    t_e, a_e = tbl.astype(orc.dtype).copy(), np.zeros((4, 1), orc.dtype)
+    for coal in (np.array([[0.75], [-1.5], [0.0]]), np.array([[-2.5], [0.25], [1.0]])):
+        orc.scatter_rowwise_adagrad(rows, coal, lr, eps, t_r, a_r)
+        orc.scatter_adagrad(rows, coal, lr, eps, t_e, a_e)
+        assert np.array_equal(t_r, t_e) and np.array_equal(a_r, a_e[:, 0])
+    # equal |G| across a row (mean of 4 equal squares is exact)
+    tbl = np.arange(20, dtype=np.float64).reshape(5, 4)
+    coal = np.array([[0.75, -0.75, 0.75, 0.75], [-1.5, 1.5, 1.5, -1.5], [0.5, 0.5, -0.5, 0.5]])
+    t_r, a_r = tbl.astype(orc.dtype).copy(), np.zeros(5, orc.dtype)
+    t_e, a_e = tbl.astype(orc.dtype).copy(), np.zeros((5, 4), orc.dtype)
+    orc.scatter_rowwise_adagrad(rows, coal, lr, eps, t_r, a_r)
+    orc.scatter_adagrad(rows, coal, lr, eps, t_e, a_e)
+    assert np.array_equal(t_r, t_e) and np.array_equal(a_r, a_e[:, 0])
+    # mean 1, eps 3: W -= lr * G / 2; then a second step adds its own mean
+    t, a = tbl.astype(orc.dtype).copy(), np.zeros(5, orc.dtype)
+    g1 = np.array([[2.0, 0, 0, 0], [0, -2.0, 0, 0], [0, 0, 0, 2.0]])
+    orc.scatter_rowwise_adagrad(rows, g1, 0.5, 3.0, t, a)
+    want = tbl.copy()
+    want[rows] -= 0.5 * g1 / 2
+    assert np.array_equal(t, want)
+    assert np.array_equal(a, np.array([1.0, 0, 1.0, 1.0, 0]))
+    # second step: G = (1, 3, 1, 3) has mean 5, A = 6, eps + A = 9
+    g2 = np.array([[1.0, 3.0, 1.0, 3.0]] * 3)
+    orc.scatter_rowwise_adagrad(rows, g2, 0.5, 3.0, t, a)
+    want[rows] -= 0.5 * g2 / 3
+    assert np.array_equal(a, np.array([6.0, 0, 6.0, 6.0, 0]))
+    tol = 6e-7 * 20 if orc.dtype == np.float32 else 1e-14 * 20
+    assert np.allclose(t, want, rtol=0, atol=tol)
+
+
 # ----------------------------------------------------------------------------
 # fp32 oracle against the fp64 oracle: a-priori rounding-error bounds
 # ----------------------------------------------------------------------------
@@ -375,4 +480,6 @@ def pin_tables_independent(orc, seeds=range(3)):
 
 ALL_PINS = [pin_worked_example, pin_tables_independent, pin_cast_matches_sorted, pin_cast_invariants,
             pin_forward_closed_form, pin_backward_closed_form, pin_brute_force,
-            pin_alg1_equals_alg3, pin_sgd_closed_form, pin_adagrad_closed_form]
+            pin_alg1_equals_alg3, pin_sgd_closed_form, pin_adagrad_closed_form,
+            pin_rmsprop_special_cases, pin_rmsprop_geometric,
+            pin_rowwise_adagrad_special_cases]

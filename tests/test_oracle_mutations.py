@@ -40,10 +40,25 @@ MUTATIONS = {
     # SGD with the sign flipped
     "sgd_sign": ("w[d] = w[d] - t;", "w[d] = w[d] + t;"),
     # Adagrad without epsilon
-    "adagrad_no_eps": ("real s = real_sqrt(reps + a[d]);", "real s = real_sqrt(a[d]);"),
+    "adagrad_no_eps": ("a[d] = a[d] + sq;\n            real s = real_sqrt(reps + a[d]);",
+                       "a[d] = a[d] + sq;\n            real s = real_sqrt(a[d]);"),
     # Adagrad dividing by the accumulator before it is updated
     "adagrad_stale_acc": ("a[d] = a[d] + sq;\n            real s = real_sqrt(reps + a[d]);",
                           "real s = real_sqrt(reps + a[d]);\n            a[d] = a[d] + sq;"),
+    # RMSprop with gamma and 1 - gamma swapped
+    "rmsprop_gamma_swapped": ("real t = rg * a[d];", "real t = rc * a[d];"),
+    # RMSprop without the (1 - gamma) factor on the new squared gradient
+    "rmsprop_no_one_minus_gamma": ("real m = rc * sq;", "real m = sq;"),
+    # RMSprop dividing by sqrt(A) without epsilon
+    "rmsprop_no_eps": ("a[d] = t + m;\n            real s = real_sqrt(reps + a[d]);",
+                       "a[d] = t + m;\n            real s = real_sqrt(a[d]);"),
+    # row-wise Adagrad adding the row's sum of squares instead of its mean
+    "rowwise_sum_not_mean": ("real m = ss / rdim;", "real m = ss;"),
+    # row-wise Adagrad squaring only the first column
+    "rowwise_first_column": ("real sq = g[d] * g[d];\n            ss = ss + sq;",
+                             "real sq = g[0] * g[0];\n            ss = ss + sq;"),
+    # row-wise Adagrad not keeping its accumulator across steps
+    "rowwise_acc_reset": ("a[0] = a[0] + m;", "a[0] = m;"),
     # expand reads the gradient of the wrong bag (off by one)
     "expand_off_by_one": ("grad_out + (int64_t)dst[j] * dim", "grad_out + (int64_t)(dst[j] > 0 ? dst[j] - 1 : 0) * dim"),
     # pairs from CSR forget the table's row offset
