@@ -71,7 +71,7 @@
 extern "C" {
 #endif
 
-#define TC_ABI_VERSION 2
+#define TC_ABI_VERSION 3
 
 typedef enum tc_status {
     TC_OK = 0,
@@ -82,8 +82,10 @@ typedef enum tc_status {
 } tc_status;
 
 typedef enum tc_opt_kind {
-    TC_OPT_SGD = 0,      /* W <- W - lr*G */
-    TC_OPT_ADAGRAD = 1   /* Eq. (2): A <- A + G*G; W <- W - lr*G/sqrt(eps + A) */
+    TC_OPT_SGD = 0,             /* W <- W - lr*G */
+    TC_OPT_ADAGRAD = 1,         /* Eq. (2): A <- A + G*G; W <- W - lr*G/sqrt(eps + A) */
+    TC_OPT_RMSPROP = 2,         /* Eq. (1): A <- gamma*A + (1-gamma)*G*G; same W step */
+    TC_OPT_ROWWISE_ADAGRAD = 3  /* Eq. (2) with one A per row, grown by mean(G*G) */
 } tc_opt_kind;
 
 /*
@@ -191,40 +193,57 @@ tc_status tc_embed_backward(const float *grad_out, int32_t num_bags, int32_t dim
                             hipStream_t stream);
 
 /*
- * Gradient scatter + optimizer (Sec. II-B; Adagrad is Eq. 2). For every
- * u < *num_unique, with r = unique_rows[u] and G = coal_grad[u, :], elementwise:
- *   TC_OPT_SGD:     t = lr*G;  W[r] = W[r] - t
- *   TC_OPT_ADAGRAD: A[r] = A[r] + G*G;  s = sqrt(eps + A[r]);  q = G/s;
+ * Gradient scatter + optimizer (Sec. II-B; RMSprop is Eq. 1, Adagrad Eq. 2).
+ * For every u < *num_unique, with r = unique_rows[u] and G = coal_grad[u, :]:
+ *   TC_OPT_SGD:     elementwise t = lr*G;  W[r] = W[r] - t
+ *   TC_OPT_ADAGRAD: elementwise A[r] = A[r] + G*G;  s = sqrt(eps + A[r]);
+ *                   q = G/s;  W[r] = W[r] - lr*q
+ *   TC_OPT_RMSPROP: elementwise t = gamma*A[r];  c = 1 - gamma;
+ *                   A[r] = t + c*(G*G);  s = sqrt(eps + A[r]);  q = G/s;
  *                   W[r] = W[r] - lr*q
+ *   TC_OPT_ROWWISE_ADAGRAD: one accumulator per row (a variant of Eq. 2
+ *                   that the paper does not define):
+ *                   m = (G_0^2 + ... + G_{dim-1}^2) / dim, summed in column
+ *                   order from +0;  A[r] = A[r] + m;  s = sqrt(eps + A[r]);
+ *                   then elementwise q = G/s;  W[r] = W[r] - lr*q
  * each a separately rounded fp32 operation (no fused multiply-add; division
- * and square root correctly rounded). Rows not in unique_rows are untouched,
- * which equals a dense update with zero gradient for these optimizers.
+ * and square root correctly rounded). Rows not in unique_rows are untouched:
+ * the update is lazy, which for SGD and both Adagrads equals a dense update
+ * with zero gradient; for RMSprop the accumulator of an untouched row is not
+ * decayed.
  *   W          [total_rows x dim] fp32 table (read-modify-write)
- *   opt_state  Adagrad accumulator A, same shape as W (read-modify-write);
- *              must be NULL for SGD
+ *   opt_state  the accumulator A (read-modify-write): [total_rows x dim] for
+ *              Adagrad and RMSprop, [total_rows] for row-wise Adagrad; must
+ *              be NULL for SGD
+ *   gamma      RMSprop's decay, in [0, 1] (TC_ERR_INVALID_ARG otherwise);
+ *              ignored by the other optimizers
  *   unique_rows must be distinct (as tc_cast_index produces them).
  */
 tc_status tc_sparse_update(float *W, float *opt_state, int64_t total_rows, int32_t dim,
                            const int32_t *unique_rows, const float *coal_grad,
                            const int32_t *num_unique, int64_t max_unique, int32_t opt_kind,
-                           float lr, float eps, hipStream_t stream);
+                           float lr, float eps, float gamma, hipStream_t stream);
 
 /*
  * Casted gradient gather-reduce (Algorithm 3) fused with the gradient
- * scatter + optimizer (Sec. II-B, Eq. 2): for every u < *num_unique, the
- * coalesced row G of tc_embed_backward is formed in registers and applied to
- * W[unique_rows[u]] (and the Adagrad accumulator) exactly as
+ * scatter + optimizer (Sec. II-B, Eqs. 1 and 2): for every u < *num_unique,
+ * the coalesced row G of tc_embed_backward is formed in registers and
+ * applied to W[unique_rows[u]] (and the accumulator) exactly as
  * tc_sparse_update applies it. The results equal those two calls bit for
  * bit; the coalesced gradient is stored to coal_grad only if that is not
  * NULL. Arguments are those of the two calls (coal_grad optional); W,
- * opt_state and grad_out must not overlap.
+ * opt_state and grad_out must not overlap. Supports TC_OPT_SGD,
+ * TC_OPT_ADAGRAD and TC_OPT_RMSPROP; TC_OPT_ROWWISE_ADAGRAD returns
+ * TC_ERR_UNSUPPORTED (a row's columns are reduced by different workgroups,
+ * so no one of them sees the whole row): use tc_embed_backward followed by
+ * tc_sparse_update for it.
  */
 tc_status tc_embed_backward_update(const float *grad_out, int32_t num_bags, int32_t dim,
                                    const int32_t *seg_offsets, const int32_t *casted_src,
                                    const int32_t *unique_rows, const int32_t *num_unique,
                                    int64_t max_unique, float *W, float *opt_state,
                                    int64_t total_rows, int32_t opt_kind, float lr, float eps,
-                                   float *coal_grad, hipStream_t stream);
+                                   float gamma, float *coal_grad, hipStream_t stream);
 
 /* Static text for a status code. */
 const char *tc_status_string(tc_status status);

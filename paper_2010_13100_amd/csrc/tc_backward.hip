@@ -72,10 +72,10 @@ constexpr int32_t kOutOfRange = 0x7ffff000;
 struct RowSink {
     float *coal;
     float *W;
-    float *A;  // Adagrad accumulator
+    float *A;  // Adagrad / RMSprop accumulator
     const int32_t *rows;
-    int32_t kind;
-    float lr, eps;
+    int32_t kind;  // TC_OPT_SGD, TC_OPT_ADAGRAD or TC_OPT_RMSPROP
+    float lr, eps, gamma, omg;  // omg = 1 - gamma
 };
 
 // One lane's column `col` of coalesced row u.
@@ -89,7 +89,10 @@ __device__ __forceinline__ void sink_value(const RowSink &k, int64_t u, int32_t 
             w = sgd_step(w, g, k.lr);
         } else {
             float a = k.A[at];
-            adagrad_step(w, a, g, k.lr, k.eps);
+            if (k.kind == TC_OPT_ADAGRAD)
+                adagrad_step(w, a, g, k.lr, k.eps);
+            else
+                rmsprop_step(w, a, g, k.lr, k.eps, k.gamma, k.omg);
             k.A[at] = a;
         }
         k.W[at] = w;
@@ -119,10 +122,17 @@ __device__ __forceinline__ void sink_group(const RowSink &k, int64_t u, int32_t 
             } else {
                 float *arow = k.A + r * dim;
                 float4 a = *reinterpret_cast<const float4 *>(arow + 4 * col4);
-                adagrad_step(w.x, a.x, g.x, k.lr, k.eps);
-                adagrad_step(w.y, a.y, g.y, k.lr, k.eps);
-                adagrad_step(w.z, a.z, g.z, k.lr, k.eps);
-                adagrad_step(w.w, a.w, g.w, k.lr, k.eps);
+                if (k.kind == TC_OPT_ADAGRAD) {
+                    adagrad_step(w.x, a.x, g.x, k.lr, k.eps);
+                    adagrad_step(w.y, a.y, g.y, k.lr, k.eps);
+                    adagrad_step(w.z, a.z, g.z, k.lr, k.eps);
+                    adagrad_step(w.w, a.w, g.w, k.lr, k.eps);
+                } else {
+                    rmsprop_step(w.x, a.x, g.x, k.lr, k.eps, k.gamma, k.omg);
+                    rmsprop_step(w.y, a.y, g.y, k.lr, k.eps, k.gamma, k.omg);
+                    rmsprop_step(w.z, a.z, g.z, k.lr, k.eps, k.gamma, k.omg);
+                    rmsprop_step(w.w, a.w, g.w, k.lr, k.eps, k.gamma, k.omg);
+                }
                 *reinterpret_cast<float4 *>(arow + 4 * col4) = a;
             }
             *reinterpret_cast<float4 *>(wrow + 4 * col4) = w;
@@ -529,7 +539,7 @@ extern "C" tc_status tc_embed_backward(const float *grad_out, int32_t num_bags, 
                TC_ERR_INVALID_ARG, "tc_embed_backward: null pointer");
     TC_REQUIRE(aligned16(grad_out) && aligned16(coal_grad), TC_ERR_UNSUPPORTED,
                "tc_embed_backward: grad_out and coal_grad must be 16-byte aligned");
-    const RowSink sink{coal_grad, nullptr, nullptr, nullptr, TC_OPT_SGD, 0.f, 0.f};
+    const RowSink sink{coal_grad, nullptr, nullptr, nullptr, TC_OPT_SGD, 0.f, 0.f, 0.f, 1.f};
     return launch_backward(grad_out, dim, casted_src, seg_offsets, num_unique, max_unique, sink,
                            stream);
 }
@@ -538,7 +548,7 @@ extern "C" tc_status tc_embed_backward_update(
     const float *grad_out, int32_t num_bags, int32_t dim, const int32_t *seg_offsets,
     const int32_t *casted_src, const int32_t *unique_rows, const int32_t *num_unique,
     int64_t max_unique, float *W, float *opt_state, int64_t total_rows, int32_t opt_kind,
-    float lr, float eps, float *coal_grad, hipStream_t stream) {
+    float lr, float eps, float gamma, float *coal_grad, hipStream_t stream) {
     clear_error();
     TC_REQUIRE(num_bags >= 0 && max_unique >= 0 && total_rows >= 0, TC_ERR_INVALID_ARG,
                "tc_embed_backward_update: negative size");
@@ -547,10 +557,15 @@ extern "C" tc_status tc_embed_backward_update(
     TC_REQUIRE(dim > 0 && dim % 4 == 0 && dim <= kMaxDim, TC_ERR_UNSUPPORTED,
                "tc_embed_backward_update: dim %d must be a multiple of 4 in [4, %d]", dim,
                kMaxDim);
-    TC_REQUIRE(opt_kind == TC_OPT_SGD || opt_kind == TC_OPT_ADAGRAD, TC_ERR_INVALID_ARG,
+    TC_REQUIRE(opt_kind >= TC_OPT_SGD && opt_kind <= TC_OPT_ROWWISE_ADAGRAD, TC_ERR_INVALID_ARG,
                "tc_embed_backward_update: unknown optimizer %d", opt_kind);
+    TC_REQUIRE(opt_kind != TC_OPT_ROWWISE_ADAGRAD, TC_ERR_UNSUPPORTED,
+               "tc_embed_backward_update: row-wise Adagrad needs whole rows; use "
+               "tc_embed_backward and tc_sparse_update");
     TC_REQUIRE((opt_kind == TC_OPT_SGD) == (opt_state == nullptr), TC_ERR_INVALID_ARG,
-               "tc_embed_backward_update: opt_state must be NULL for SGD and given for Adagrad");
+               "tc_embed_backward_update: opt_state must be NULL for SGD and given otherwise");
+    TC_REQUIRE(opt_kind != TC_OPT_RMSPROP || (gamma >= 0.f && gamma <= 1.f), TC_ERR_INVALID_ARG,
+               "tc_embed_backward_update: RMSprop gamma must lie in [0, 1]");
     if (max_unique == 0) return TC_OK;
     TC_REQUIRE(grad_out && seg_offsets && casted_src && unique_rows && num_unique && W,
                TC_ERR_INVALID_ARG, "tc_embed_backward_update: null pointer");
@@ -558,7 +573,8 @@ extern "C" tc_status tc_embed_backward_update(
                    (!coal_grad || aligned16(coal_grad)),
                TC_ERR_UNSUPPORTED,
                "tc_embed_backward_update: float pointers must be 16-byte aligned");
-    const RowSink sink{coal_grad, W, opt_state, unique_rows, opt_kind, lr, eps};
+    const RowSink sink{coal_grad, W, opt_state, unique_rows, opt_kind, lr, eps, gamma,
+                       1.0f - gamma};
     return launch_backward(grad_out, dim, casted_src, seg_offsets, num_unique, max_unique, sink,
                            stream);
 }
@@ -599,7 +615,7 @@ extern "C" tc_status tc_embed_coalesce(const float *expanded, int64_t num_pairs,
                "tc_embed_coalesce: expanded and coal_grad must be 16-byte aligned");
     // Algorithm 1's accumulate is the casted gather-reduce over the expanded
     // rows, in sorted order: the same kernels with sorted positions as ids.
-    const RowSink sink{coal_grad, nullptr, nullptr, nullptr, TC_OPT_SGD, 0.f, 0.f};
+    const RowSink sink{coal_grad, nullptr, nullptr, nullptr, TC_OPT_SGD, 0.f, 0.f, 0.f, 1.f};
     return launch_backward(expanded, dim, sorted_pos, seg_offsets, num_unique, max_unique, sink,
                            stream);
 }

@@ -18,4 +18,13 @@ __device__ __forceinline__ void adagrad_step(float &w, float &a, float g, float 
     w = w - lr * (g / sqrtf(eps + a));
 }
 
+// RMSprop, Eq. (1): A <- gamma*A + (1 - gamma)*G*G; W <- W - lr * (G /
+// sqrt(eps + A)). `omg` is 1 - gamma, rounded once by the caller.
+__device__ __forceinline__ void rmsprop_step(float &w, float &a, float g, float lr, float eps,
+                                             float gamma, float omg) {
+    const float t = gamma * a;
+    a = t + omg * (g * g);
+    w = w - lr * (g / sqrtf(eps + a));
+}
+
 }  // namespace tc

@@ -15,8 +15,9 @@ import torch
 from . import build as _build
 
 TC_OK, TC_ERR_INVALID_ARG, TC_ERR_UNSUPPORTED, TC_ERR_WORKSPACE, TC_ERR_HIP = range(5)
-TC_OPT_SGD, TC_OPT_ADAGRAD = 0, 1
-OPTIMIZERS = {"sgd": TC_OPT_SGD, "adagrad": TC_OPT_ADAGRAD}
+TC_OPT_SGD, TC_OPT_ADAGRAD, TC_OPT_RMSPROP, TC_OPT_ROWWISE_ADAGRAD = range(4)
+OPTIMIZERS = {"sgd": TC_OPT_SGD, "adagrad": TC_OPT_ADAGRAD, "rmsprop": TC_OPT_RMSPROP,
+              "rowwise_adagrad": TC_OPT_ROWWISE_ADAGRAD}
 
 _vp, _i32, _i64, _f32, _sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
                               ctypes.c_size_t)
@@ -28,9 +29,9 @@ _SIGNATURES = {
                              _vp, _vp, _sz, _vp]),
     "tc_embed_backward": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _i64, _vp, _vp]),
     "tc_sparse_update": (_i32, [_vp, _vp, _i64, _i32, _vp, _vp, _vp, _i64, _i32, _f32, _f32,
-                                _vp]),
+                                _f32, _vp]),
     "tc_embed_backward_update": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _vp,
-                                        _i64, _i32, _f32, _f32, _vp, _vp]),
+                                        _i64, _i32, _f32, _f32, _f32, _vp, _vp]),
     "tc_argsort_rows": (_i32, [_vp, _i32, _i32, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp,
                                _vp, _sz, _vp]),
     "tc_embed_expand": (_i32, [_vp, _i32, _i32, _vp, _i64, _vp, _vp]),
@@ -127,23 +128,23 @@ def tc_embed_backward(grad_out, seg_offsets, casted_src, num_unique, max_unique,
 
 
 def tc_sparse_update(W, opt_state, unique_rows, coal_grad, num_unique, max_unique, opt_kind, lr,
-                     eps, stream=None) -> None:
+                     eps, gamma=0.0, stream=None) -> None:
     _check(_lib.tc_sparse_update(
         _ptr(W, torch.float32, "W"), _ptr(opt_state, torch.float32, "opt_state"), W.shape[0],
         W.shape[1], _ptr(unique_rows, torch.int32, "unique_rows"),
         _ptr(coal_grad, torch.float32, "coal_grad"), _ptr(num_unique, torch.int32, "num_unique"),
-        max_unique, opt_kind, lr, eps, _stream(stream)), "tc_sparse_update")
+        max_unique, opt_kind, lr, eps, gamma, _stream(stream)), "tc_sparse_update")
 
 
 def tc_embed_backward_update(grad_out, seg_offsets, casted_src, unique_rows, num_unique,
-                             max_unique, W, opt_state, opt_kind, lr, eps, coal_grad=None,
-                             stream=None) -> None:
+                             max_unique, W, opt_state, opt_kind, lr, eps, gamma=0.0,
+                             coal_grad=None, stream=None) -> None:
     _check(_lib.tc_embed_backward_update(
         _ptr(grad_out, torch.float32, "grad_out"), grad_out.shape[0], grad_out.shape[1],
         _ptr(seg_offsets, torch.int32, "seg_offsets"), _ptr(casted_src, torch.int32, "casted_src"),
         _ptr(unique_rows, torch.int32, "unique_rows"), _ptr(num_unique, torch.int32, "num_unique"),
         max_unique, _ptr(W, torch.float32, "W"), _ptr(opt_state, torch.float32, "opt_state"),
-        W.shape[0], opt_kind, lr, eps, _ptr(coal_grad, torch.float32, "coal_grad"),
+        W.shape[0], opt_kind, lr, eps, gamma, _ptr(coal_grad, torch.float32, "coal_grad"),
         _stream(stream)), "tc_embed_backward_update")
 
 
@@ -186,7 +187,7 @@ class EmbeddingTrainer:
 
     def __init__(self, *, total_rows: int, dim: int, num_tables: int, bags_per_table: int,
                  max_pairs: int, optimizer: str = "sgd", lr: float = 0.01, eps: float = 1e-8,
-                 device="cuda", table: torch.Tensor | None = None, max_table_rows: int = 0):
+                 gamma: float = 0.99, device="cuda", table: torch.Tensor | None = None, max_table_rows: int = 0):
         self.total_rows, self.dim = total_rows, dim
         self.num_tables, self.bags_per_table = num_tables, bags_per_table
         self.num_bags = num_tables * bags_per_table
@@ -194,11 +195,16 @@ class EmbeddingTrainer:
         self.max_table_rows = max_table_rows
         self.max_unique = min(max_pairs, total_rows)
         self.opt_kind = OPTIMIZERS[optimizer]
-        self.lr, self.eps = lr, eps
+        self.lr, self.eps, self.gamma = lr, eps, gamma
         i32 = dict(dtype=torch.int32, device=device)
         self.W = table if table is not None else torch.empty((total_rows, dim), dtype=torch.float32,
                                                              device=device)
-        self.A = (torch.zeros_like(self.W) if self.opt_kind == TC_OPT_ADAGRAD else None)
+        if self.opt_kind in (TC_OPT_ADAGRAD, TC_OPT_RMSPROP):
+            self.A = torch.zeros_like(self.W)
+        elif self.opt_kind == TC_OPT_ROWWISE_ADAGRAD:
+            self.A = torch.zeros(total_rows, dtype=torch.float32, device=self.W.device)
+        else:
+            self.A = None
         self.out = torch.empty((self.num_bags, dim), dtype=torch.float32, device=device)
         self.unique_rows = torch.empty(max(self.max_unique, 1), **i32)
         self.seg_offsets = torch.empty(self.max_unique + 1, **i32)
@@ -226,7 +232,7 @@ class EmbeddingTrainer:
 
     def update(self, stream=None):
         tc_sparse_update(self.W, self.A, self.unique_rows, self.coal, self.num_unique,
-                         self.max_unique, self.opt_kind, self.lr, self.eps, stream)
+                         self.max_unique, self.opt_kind, self.lr, self.eps, self.gamma, stream)
 
     def baseline_backward(self, table_row_offset, indices, bag_offsets, num_pairs, grad_out,
                           stream=None):
@@ -249,15 +255,16 @@ class EmbeddingTrainer:
         """backward + update in one pass (coal stored only if store_coal)."""
         tc_embed_backward_update(grad_out, self.seg_offsets, self.casted_src, self.unique_rows,
                                  self.num_unique, self.max_unique, self.W, self.A, self.opt_kind,
-                                 self.lr, self.eps, self.coal if store_coal else None, stream)
+                                 self.lr, self.eps, self.gamma,
+                                 self.coal if store_coal else None, stream)
 
     def step(self, table_row_offset, indices, bag_offsets, num_pairs, grad_out, stream=None,
              fused=True):
         """forward + cast + backward + update, stream-ordered; with fused the
-        last two are one call."""
+        last two are one call (row-wise Adagrad always takes the two calls)."""
         self.forward(table_row_offset, indices, bag_offsets, stream)
         self.cast(table_row_offset, indices, bag_offsets, num_pairs, stream)
-        if fused:
+        if fused and self.opt_kind != TC_OPT_ROWWISE_ADAGRAD:
             self.backward_update(grad_out, stream)
         else:
             self.backward(grad_out, stream)

@@ -56,9 +56,10 @@ class Workload:
     pooling_value: int         # fixed length, or Poisson mean (min length 1)
     dist: str                  # "uniform" | "zipf"
     alpha: float = 0.0         # Zipf exponent
-    optimizer: str = "sgd"     # "sgd" | "adagrad"
+    optimizer: str = "sgd"     # "sgd" | "adagrad" | "rmsprop" | "rowwise_adagrad"
     lr: float = 0.01
     eps: float = 1e-8
+    gamma: float = 0.99        # RMSprop decay (Eq. 1)
     init_lo: float = -0.01
     init_hi: float = 0.01
 
@@ -71,10 +72,12 @@ class Workload:
         return self.num_tables * self.rows_per_table
 
     def scaled(self, *, name=None, num_tables=None, rows_per_table=None,
-               dim=None, batch=None, pooling_value=None) -> "Workload":
-        """The same distributions at a smaller (or different) shape."""
+               dim=None, batch=None, pooling_value=None, optimizer=None) -> "Workload":
+        """The same distributions at a smaller (or different) shape, optionally
+        with another optimizer."""
         return dataclasses.replace(
             self,
+            optimizer=optimizer or self.optimizer,
             name=name or (self.name + "-scaled"),
             num_tables=num_tables or self.num_tables,
             rows_per_table=rows_per_table or self.rows_per_table,
@@ -82,6 +85,20 @@ class Workload:
             batch=batch or self.batch,
             pooling_value=pooling_value or self.pooling_value,
         )
+
+
+def variant(w: Workload, *, batch=None, dim=None, optimizer=None) -> Workload:
+    """w with another batch size, dimension or optimizer (w itself if none
+    changes), renamed to match: the name's -d, -b and optimizer fields."""
+    if ((batch is None or batch == w.batch) and (dim is None or dim == w.dim)
+            and (optimizer is None or optimizer == w.optimizer)):
+        return w
+    parts = w.name.split("-")
+    batch, dim, optimizer = batch or w.batch, dim or w.dim, optimizer or w.optimizer
+    parts = [f"d{dim}" if p == f"d{w.dim}" else f"b{batch}" if p == f"b{w.batch}" else p
+             for p in parts[:-1]] + [optimizer]
+    return dataclasses.replace(w, name="-".join(parts), batch=batch, dim=dim,
+                               optimizer=optimizer)
 
 
 # The five workloads of the measurement plan, named by what they are.

@@ -52,7 +52,7 @@ class GpuRun:
         self.trainer = tc.EmbeddingTrainer(
             total_rows=w.total_rows, dim=w.dim, num_tables=w.num_tables,
             bags_per_table=w.batch, max_pairs=max_pairs, optimizer=w.optimizer, lr=w.lr,
-            eps=w.eps,
+            eps=w.eps, gamma=w.gamma,
             max_table_rows=w.rows_per_table if max_table_rows is None else max_table_rows)
         if table is not None:
             self.trainer.W.copy_(torch.from_numpy(table))
@@ -118,7 +118,12 @@ class OracleModel:
         self.ids = np.asarray(row_ids, np.int64)
         self.table = (wl.table_rows(w, self.ids) if table_vals is None
                       else np.array(table_vals, np.float32, copy=True))
-        self.acc = np.zeros_like(self.table) if w.optimizer == "adagrad" else None
+        if w.optimizer in ("adagrad", "rmsprop"):
+            self.acc = np.zeros_like(self.table)
+        elif w.optimizer == "rowwise_adagrad":
+            self.acc = np.zeros(len(self.ids), np.float32)
+        else:
+            self.acc = None
 
     def step(self, b: wl.Batch):
         w, o = self.w, self.orc
@@ -127,15 +132,27 @@ class OracleModel:
         out = o.forward(src, dst, w.num_bags, self.table, self.ids)
         cast = o.tensor_casting(src, dst)
         coal, rows = o.coalesce(src, o.expand(dst, b.grad_out))
-        if w.optimizer == "sgd":
-            o.scatter_sgd(rows, coal, np.float32(w.lr), self.table, self.ids)
-        else:
-            o.scatter_adagrad(rows, coal, np.float32(w.lr), np.float32(w.eps), self.table,
-                              self.acc, self.ids)
+        scatter(o, w, rows, coal, self.table, self.acc, self.ids)
         return out, cast, coal, rows
 
     def rows(self, ids):
         return self.table[np.searchsorted(self.ids, ids)]
+
+
+def scatter(o: oracle.Oracle, w: wl.Workload, rows, coal, table, acc, ids):
+    """The oracle's update with w's optimizer, its constants rounded to fp32
+    as the library receives them."""
+    lr, eps, gamma = np.float32(w.lr), np.float32(w.eps), np.float32(w.gamma)
+    if w.optimizer == "sgd":
+        o.scatter_sgd(rows, coal, lr, table, ids)
+    elif w.optimizer == "adagrad":
+        o.scatter_adagrad(rows, coal, lr, eps, table, acc, ids)
+    elif w.optimizer == "rmsprop":
+        o.scatter_rmsprop(rows, coal, lr, eps, gamma, table, acc, ids)
+    elif w.optimizer == "rowwise_adagrad":
+        o.scatter_rowwise_adagrad(rows, coal, lr, eps, table, acc, ids)
+    else:
+        raise ValueError(w.optimizer)
 
 
 def compare_cast(got: dict, ref: dict, n: int):

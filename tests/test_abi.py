@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(header):
 
 
 def test_version_and_status_strings(tc):
-    assert tc.tc_abi_version() == 2
+    assert tc.tc_abi_version() == 3
     lib = tc._lib
     for code, name in enumerate(["TC_OK", "TC_ERR_INVALID_ARG", "TC_ERR_UNSUPPORTED",
                                  "TC_ERR_WORKSPACE", "TC_ERR_HIP"]):
@@ -152,10 +152,20 @@ def test_backward_and_update_reject_bad_arguments(tc):
         return lib.tc_sparse_update(k.get("W", h.fp()), k.get("A", None), k.get("rows", 100),
                                     k.get("dim", 8), k.get("ur", h.ip()), k.get("coal", h.fp()),
                                     k.get("nu", h.ip()), k.get("mu", 10), k.get("opt", 0),
-                                    0.01, 1e-8, None)
+                                    0.01, 1e-8, k.get("gamma", 0.9), None)
     assert upd(A=h.fp()) == tc.TC_ERR_INVALID_ARG               # SGD takes no state
     assert upd(opt=1) == tc.TC_ERR_INVALID_ARG                  # Adagrad needs state
+    assert upd(opt=2) == tc.TC_ERR_INVALID_ARG                  # RMSprop needs state
+    assert upd(opt=3) == tc.TC_ERR_INVALID_ARG                  # row-wise Adagrad too
+    assert upd(opt=2, A=h.fp(), gamma=1.5) == tc.TC_ERR_INVALID_ARG
+    assert upd(opt=2, A=h.fp(), gamma=-0.25) == tc.TC_ERR_INVALID_ARG
+    assert upd(opt=2, A=h.fp(), gamma=float("nan")) == tc.TC_ERR_INVALID_ARG
+    assert "gamma" in _err(tc)
+    assert upd(opt=4, A=h.fp()) == tc.TC_ERR_INVALID_ARG
+    assert upd(opt=-1, A=h.fp()) == tc.TC_ERR_INVALID_ARG
+    assert upd(opt=2, A=h.fp(misalign=True)) == tc.TC_ERR_UNSUPPORTED
     assert upd(opt=7) == tc.TC_ERR_INVALID_ARG
+    assert upd(opt=2, A=h.fp(), mu=0) == tc.TC_OK
     assert upd(dim=3) == tc.TC_ERR_UNSUPPORTED
     assert upd(ur=None) == tc.TC_ERR_INVALID_ARG
     assert upd(opt=1, A=h.fp(misalign=True)) == tc.TC_ERR_UNSUPPORTED
@@ -165,13 +175,17 @@ def test_backward_and_update_reject_bad_arguments(tc):
             k.get("g", h.fp()), k.get("nb", 10), k.get("dim", 8), k.get("so", h.ip()),
             k.get("cs", h.ip()), k.get("ur", h.ip()), k.get("nu", h.ip()), k.get("mu", 10),
             k.get("W", h.fp()), k.get("A", None), k.get("rows", 100), k.get("opt", 0), 0.01, 1e-8,
-            k.get("coal", None), None)
+            k.get("gamma", 0.9), k.get("coal", None), None)
     assert fused(dim=6) == tc.TC_ERR_UNSUPPORTED
     assert fused(mu=-1) == tc.TC_ERR_INVALID_ARG
     assert fused(rows=2 ** 31) == tc.TC_ERR_INVALID_ARG
     assert fused(A=h.fp()) == tc.TC_ERR_INVALID_ARG             # SGD takes no state
     assert fused(opt=1) == tc.TC_ERR_INVALID_ARG                # Adagrad needs state
-    assert fused(opt=2, A=h.fp()) == tc.TC_ERR_INVALID_ARG
+    assert fused(opt=2) == tc.TC_ERR_INVALID_ARG                # RMSprop needs state
+    assert fused(opt=2, A=h.fp(), gamma=2.0) == tc.TC_ERR_INVALID_ARG
+    assert fused(opt=3, A=h.fp()) == tc.TC_ERR_UNSUPPORTED      # row-wise: two calls
+    assert "row-wise" in _err(tc)
+    assert fused(opt=5, A=h.fp()) == tc.TC_ERR_INVALID_ARG
     assert fused(W=None) == tc.TC_ERR_INVALID_ARG and "null" in _err(tc)
     assert fused(ur=None) == tc.TC_ERR_INVALID_ARG
     assert fused(coal=h.fp(misalign=True)) == tc.TC_ERR_UNSUPPORTED

@@ -1,0 +1,82 @@
+"""The optimizer variants on the GPU against the CPU oracle: RMSprop (Eq. 1)
+through tc_sparse_update and through the fused tc_embed_backward_update, and
+row-wise Adagrad through tc_sparse_update, over three steps so that the
+accumulator's history enters the result. Tables and accumulators must match
+the fp32 oracle bit for bit (both sides take the same separately rounded
+fp32 operations in the same order)."""
+import numpy as np
+import pytest
+
+from paper_2010_13100_amd import workload as wl
+from tests.gpu_harness import GpuRun, OracleModel, assert_close
+
+pytestmark = pytest.mark.gpu
+
+W = wl.WORKLOADS
+
+
+def global_rows(w, b):
+    t = np.repeat(np.arange(w.num_bags) // w.batch, np.diff(b.bag_offsets))
+    return b.table_row_offset[t] + b.indices
+
+
+def run_steps(w, fused, steps=3):
+    batches = [wl.make_batch(w, s) for s in range(steps)]
+    touched = np.unique(np.concatenate([global_rows(w, b) for b in batches]))
+    print(f"\n[{w.name} {w.optimizer} gamma={w.gamma} fused={fused}] pairs "
+          f"{[b.num_pairs for b in batches]} touched {len(touched)}", flush=True)
+    run = GpuRun(w, max_pairs=max(b.num_pairs for b in batches))
+    model = OracleModel(w, touched)
+    for b in batches:
+        out, cast, coal = run.step(b, fused=fused)
+        _, r_cast, r_coal, r_rows = model.step(b)
+        assert np.array_equal(cast["unique_rows"], r_rows)
+        assert_close(coal, r_coal, "coalesced gradient", bitwise=True)
+    assert_close(run.rows(touched), model.table, "updated table rows", bitwise=True)
+    acc = run.acc_rows(touched)
+    assert_close(acc.reshape(len(touched), -1), model.acc.reshape(len(touched), -1),
+                 f"{w.optimizer} accumulator", bitwise=True)
+    rng = np.random.default_rng(1)
+    untouched = np.setdiff1d(rng.integers(0, w.total_rows, size=4000), touched)
+    assert np.array_equal(run.rows(untouched), wl.table_rows(w, untouched))
+    assert not np.any(run.acc_rows(untouched))
+    run.release()
+
+
+# Zipf-skewed pairs (segments long enough for the multi-workgroup backward)
+# and uniform ones, over several sort tiles with a ragged last tile.
+SHAPES = {
+    "c3-2x50k": W["c3"].scaled(name="c3-2x50k", num_tables=2, rows_per_table=50_000, batch=256),
+    "c2-2x20k": W["c2"].scaled(name="c2-2x20k", num_tables=2, rows_per_table=20_000, batch=256),
+    "c4-2x20k": W["c4"].scaled(name="c4-2x20k", num_tables=2, rows_per_table=20_000, batch=513),
+}
+
+
+@pytest.mark.parametrize("fused", [True, False])
+@pytest.mark.parametrize("shape", list(SHAPES))
+def test_rmsprop(shape, fused):
+    run_steps(SHAPES[shape].scaled(optimizer="rmsprop"), fused)
+
+
+@pytest.mark.parametrize("gamma", [0.0, 1.0, 0.5])
+def test_rmsprop_gamma_ends(gamma):
+    import dataclasses
+    w = dataclasses.replace(SHAPES["c3-2x50k"], optimizer="rmsprop", gamma=gamma)
+    run_steps(w, fused=True, steps=2)
+
+
+@pytest.mark.parametrize("shape", list(SHAPES))
+def test_rowwise_adagrad(shape):
+    # row-wise Adagrad takes backward and update as two calls
+    run_steps(SHAPES[shape].scaled(optimizer="rowwise_adagrad"), fused=False)
+
+
+@pytest.mark.parametrize("dim", [4, 8, 12, 32, 100, 252, 260, 512, 1024])
+@pytest.mark.parametrize("opt", ["rmsprop", "rowwise_adagrad"])
+def test_dims(opt, dim):
+    # every lane-group shape of the update kernel, including partial chunks
+    w = W["c3"].scaled(name=f"d{dim}", num_tables=1, rows_per_table=3000, dim=dim, batch=97,
+                       optimizer=opt)
+    run_steps(w, fused=False, steps=2)
+    if opt == "rmsprop":
+        run_steps(w, fused=True, steps=2)
