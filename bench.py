@@ -119,7 +119,7 @@ def run_ab(args, w, trainer, dbat, stream):
     # gather-reduce reads N (gathered) rows and writes U rows
     base_bytes = nb * D4 + n * D4 + n * D4 + u * D4 + 3 * n * 4
     cast_bytes = n * D4 + u * D4 + 2 * n * 4
-    print(json.dumps({
+    return {
         "metric": "backward A/B: baseline expand-coalesce vs Tensor Casting, us per step",
         "config": {"workload": f"{args.config}: {w.name}", "pairs_per_step": round(n, 1),
                    "unique_rows_per_step": round(u, 1)},
@@ -130,7 +130,7 @@ def run_ab(args, w, trainer, dbat, stream):
         "algorithmic_bytes": {"baseline": round(base_bytes), "casted": round(cast_bytes),
                               "ratio": round(base_bytes / cast_bytes, 3)},
         "note": "both variants include their sort (argsort / cast); dtype f32; data synthetic",
-    }), flush=True)
+    }
 
 
 def write_traffic(pmc_dir: str, workload: str, calls) -> dict:
@@ -222,84 +222,37 @@ def cpu_baseline(w, batch, budget_s: float):
             "seconds_per_phase": {k: round(v / steps, 4) for k, v in phases.items()}}
 
 
-def main():
-    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
-    ap.add_argument("--cpu-budget", type=float, default=15.0,
-                    help="seconds of oracle work for cpu_baseline (0 disables)")
-    ap.add_argument("--ab", action="store_true",
-                    help="instead of the step: time the paper's baseline backward "
-                         "(expand-coalesce) against the casted backward and exit")
-    ap.add_argument("--unfused", action="store_true",
-                    help="backward and update as two calls (tc_embed_backward, tc_sparse_update)")
-    ap.add_argument("--optimizer", default=None,
-                    choices=["sgd", "adagrad", "rmsprop", "rowwise_adagrad"],
-                    help="replace the workload's optimizer (row-wise Adagrad runs unfused)")
-    ap.add_argument("--batch", type=int, default=None,
-                    help="replace the workload's bags per table (sensitivity sweep)")
-    ap.add_argument("--dim", type=int, default=None,
-                    help="replace the workload's embedding dimension (sensitivity sweep)")
-    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
-                    help="only run 5 plain device copies of BYTES bytes (scale for the HBM "
-                         "byte counters) and exit")
-    ap.add_argument("--traffic-from", metavar="PMC_DIR", default=None,
-                    help="write profiles/traffic.json entries for --config from rocprofv3 "
-                         "counter runs in PMC_DIR and exit (no GPU needed)")
-    args = ap.parse_args()
-    if args.traffic_from:
-        calls = ["forward", "backward", "update"] if args.unfused else ["forward", "backward_update"]
-        print(json.dumps(write_traffic(args.traffic_from, args.config, calls), indent=1))
-        return
-    if args.copy_calibration:
-        import torch
-        src = torch.ones(args.copy_calibration // 4, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        for _ in range(5):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        print(json.dumps({"copy_calibration_bytes": args.copy_calibration, "copies": 5}))
-        return
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the hot path is built and timed on a single "
-              "MI355X; run with --gpus 1", file=sys.stderr)
-        sys.exit(2)
-
-    import numpy as np
+def setup(w, dev):
+    """Batches, a trainer with a filled table, and device copies of the
+    batches for workload w."""
     import torch
 
     from paper_2010_13100_amd import device_fill, tc
     from paper_2010_13100_amd import workload as wl
 
-    w = wl.WORKLOADS[args.config]
-    variant = wl.variant(w, batch=args.batch, dim=args.dim, optimizer=args.optimizer)
-    traffic_key = args.config if variant is w else None
-    w = variant
-    if w.optimizer == "rowwise_adagrad":
-        args.unfused = True
-    print(f"[bench] workload {args.config} {w.name}: generating {NUM_BATCHES} batches",
-          file=sys.stderr, flush=True)
+    print(f"[bench] workload {w.name}: generating {NUM_BATCHES} batches", file=sys.stderr,
+          flush=True)
     batches = [wl.make_batch(w, step=s) for s in range(NUM_BATCHES)]
     max_pairs = max(b.num_pairs for b in batches)
-    dev = torch.device("cuda", 0)
     trainer = tc.EmbeddingTrainer(total_rows=w.total_rows, dim=w.dim, num_tables=w.num_tables,
                                   bags_per_table=w.batch, max_pairs=max_pairs,
                                   optimizer=w.optimizer, lr=w.lr, eps=w.eps, gamma=w.gamma,
-                                  device=dev,
-                                  max_table_rows=w.rows_per_table)
+                                  device=dev, max_table_rows=w.rows_per_table)
     device_fill.fill_uniform(trainer.W, seed=0, lo=w.init_lo, hi=w.init_hi)
     dbat = [dict(off=torch.from_numpy(b.table_row_offset).to(dev),
                  idx=torch.from_numpy(b.indices).to(dev),
                  bo=torch.from_numpy(b.bag_offsets).to(dev),
                  grad=torch.from_numpy(b.grad_out).to(dev), n=b.num_pairs) for b in batches]
-    stream = torch.cuda.current_stream(dev)
-    if args.ab:
-        run_ab(args, w, trainer, dbat, stream)
-        return
+    return batches, trainer, dbat
 
-    calls = (["forward", "cast", "backward", "update"] if args.unfused
+
+def measure_step(args, w, cfg_name, trainer, dbat, stream, unfused, traffic_key):
+    """Time args.steps steps (after args.warmup) and return the result line
+    (without cpu_baseline)."""
+    import numpy as np
+    import torch
+
+    calls = (["forward", "cast", "backward", "update"] if unfused
              else ["forward", "cast", "backward_update"])
     fns = {"forward": lambda d: trainer.forward(d["off"], d["idx"], d["bo"], stream),
            "cast": lambda d: trainer.cast(d["off"], d["idx"], d["bo"], d["n"], stream),
@@ -370,7 +323,7 @@ def main():
     achieved = nbytes[dom] / (dom_ms * 1e-3) / 1e9
     traffic = None if traffic_key is None else load_traffic(dom, traffic_key)
     traffic_gbs = None if traffic is None else traffic / (dom_ms * 1e-3) / 1e9
-    result = {
+    return {
         "metric": "embedding train steps/sec (fwd+cast+bwd+update) and achieved HBM GB/s",
         "value": round(args.steps / (ms_total * 1e-3), 3),
         "unit": "steps/s",
@@ -384,7 +337,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic (seeded Zipf/uniform index streams, N(0,1) output gradients, "
                 "SplitMix64 table init)",
-        "config": {"workload": f"{args.config}: {w.name}", "tables": w.num_tables,
+        "config": {"workload": f"{cfg_name}: {w.name}", "tables": w.num_tables,
                    "rows_per_table": w.rows_per_table, "dim": w.dim, "batch": w.batch,
                    "pairs_per_step": round(float(np.mean([d["n"] for d in dbat])), 1),
                    "unique_rows_per_step": round(float(np.mean(uniq)), 1),
@@ -407,6 +360,111 @@ def main():
                      "traffic_frac": None if traffic_gbs is None
                      else round(traffic_gbs / HBM_PEAK_GBS, 4)},
     }
+
+
+def run_sweep(args, base, cfg_name, dev):
+    """The sensitivity study (Sec. VI-E): for each batch size or embedding
+    dimension, the step (steps/s, dominant call's HBM fraction) and the
+    backward A/B (baseline expand-coalesce against Tensor Casting). One JSON
+    line per point."""
+    import torch
+
+    from paper_2010_13100_amd import workload as wl
+
+    what, _, values = args.sweep.partition("=")
+    if what not in ("batch", "dim") or not values:
+        raise SystemExit("--sweep takes batch=B1,B2,... or dim=D1,D2,...")
+    for v in (int(x) for x in values.split(",")):
+        w = wl.variant(base, **{what: v})
+        _, trainer, dbat = setup(w, dev)
+        stream = torch.cuda.current_stream(dev)
+        unfused = args.unfused or w.optimizer == "rowwise_adagrad"
+        res = measure_step(args, w, cfg_name, trainer, dbat, stream, unfused, None)
+        ab = run_ab(args, w, trainer, dbat, stream)
+        print(json.dumps({
+            "sweep": what, what: v, "workload": w.name,
+            "pairs_per_step": res["config"]["pairs_per_step"],
+            "unique_rows_per_step": res["config"]["unique_rows_per_step"],
+            "steps_per_s": res["value"], "ms_per_step": res["ms_per_step"],
+            "per_call_us": res["per_call_us"],
+            "dominant_call": res["roofline"]["call"],
+            "dominant_frac_of_hbm_peak": res["roofline"]["frac"],
+            "step_algorithmic_frac_of_hbm_peak": res["step_algorithmic_frac_of_hbm_peak"],
+            "ab_baseline_us": ab["baseline_us"], "ab_casted_us": ab["casted_us"],
+            "ab_speedup": ab["speedup"], "ab_bytes_ratio": ab["algorithmic_bytes"]["ratio"],
+            "steps": args.steps, "warmup": args.warmup}), flush=True)
+        del trainer, dbat
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="seconds of oracle work for cpu_baseline (0 disables)")
+    ap.add_argument("--ab", action="store_true",
+                    help="instead of the step: time the paper's baseline backward "
+                         "(expand-coalesce) against the casted backward and exit")
+    ap.add_argument("--unfused", action="store_true",
+                    help="backward and update as two calls (tc_embed_backward, tc_sparse_update)")
+    ap.add_argument("--optimizer", default=None,
+                    choices=["sgd", "adagrad", "rmsprop", "rowwise_adagrad"],
+                    help="replace the workload's optimizer (row-wise Adagrad runs unfused)")
+    ap.add_argument("--batch", type=int, default=None,
+                    help="replace the workload's bags per table")
+    ap.add_argument("--dim", type=int, default=None,
+                    help="replace the workload's embedding dimension")
+    ap.add_argument("--sweep", default=None, metavar="batch=B1,B2,..|dim=D1,D2,..",
+                    help="sensitivity sweep: step and backward A/B per value, one JSON line "
+                         "each, then exit")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run 5 plain device copies of BYTES bytes (scale for the HBM "
+                         "byte counters) and exit")
+    ap.add_argument("--traffic-from", metavar="PMC_DIR", default=None,
+                    help="write profiles/traffic.json entries for --config from rocprofv3 "
+                         "counter runs in PMC_DIR and exit (no GPU needed)")
+    args = ap.parse_args()
+    if args.traffic_from:
+        calls = ["forward", "backward", "update"] if args.unfused else ["forward", "backward_update"]
+        print(json.dumps(write_traffic(args.traffic_from, args.config, calls), indent=1))
+        return
+    if args.copy_calibration:
+        import torch
+        src = torch.ones(args.copy_calibration // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": args.copy_calibration, "copies": 5}))
+        return
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the hot path is built and timed on a single "
+              "MI355X; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2010_13100_amd import workload as wl
+
+    dev = torch.device("cuda", 0)
+    w = wl.WORKLOADS[args.config]
+    variant = wl.variant(w, batch=args.batch, dim=args.dim, optimizer=args.optimizer)
+    traffic_key = args.config if variant is w else None
+    w = variant
+    if args.sweep:
+        run_sweep(args, w, args.config, dev)
+        return
+    batches, trainer, dbat = setup(w, dev)
+    stream = torch.cuda.current_stream(dev)
+    if args.ab:
+        print(json.dumps(run_ab(args, w, trainer, dbat, stream)), flush=True)
+        return
+    unfused = args.unfused or w.optimizer == "rowwise_adagrad"
+    result = measure_step(args, w, args.config, trainer, dbat, stream, unfused, traffic_key)
     if args.cpu_budget > 0:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, batches[0], args.cpu_budget)

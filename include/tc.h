@@ -9,7 +9,8 @@
  *   tc_embed_forward   embedding gather-reduce (Sec. II-B): pooled row sums
  *   tc_cast_index      Tensor Casting (Algorithm 2, Sec. IV-A)
  *   tc_embed_backward  casted gradient gather-reduce (Algorithm 3)
- *   tc_sparse_update   gradient scatter with SGD or Adagrad (Sec. II-B, Eq. 2)
+ *   tc_sparse_update   gradient scatter with SGD, Adagrad (Eq. 2) or RMSprop
+ *                      (Eq. 1), Sec. II-B
  *
  * tc_embed_backward_update does the last two in one pass (same results bit
  * for bit) without storing the coalesced gradient in device memory.
@@ -25,8 +26,9 @@
  * Pointers are DEVICE pointers owned by the caller unless a comment says
  * "host". The library never allocates or frees device memory, never
  * synchronises the stream and never copies to the host; scratch memory comes
- * from the caller's workspace (tc_cast_workspace_bytes). Buffers must stay
- * alive until the stream has finished the call.
+ * from the caller's workspaces (tc_cast_workspace_bytes,
+ * tc_backward_workspace_bytes). Buffers must stay alive until the stream has
+ * finished the call.
  *
  * Every call is asynchronous on `stream` (a hipStream_t; NULL is the legacy
  * default stream) and returns a tc_status. Host-side argument checks run
@@ -53,8 +55,10 @@
  *
  * Arithmetic: fp32 values, fp32 accumulation. Sums are taken one term after
  * another, from +0, in the order of the index array (forward) or of the
- * casted index (backward); results do not depend on the launch configuration
- * and repeat bit for bit.
+ * casted index (backward). The one exception is opt-in: given a backward
+ * workspace, the backward sums a segment of TC_BACKWARD_SPLIT_PAIRS pairs or
+ * more in pieces (see tc_embed_backward). Either way results do not depend
+ * on the launch configuration and repeat bit for bit.
  *
  * Thread safety: no global state besides the per-thread error message;
  * concurrent calls on different streams with different buffers are safe.
@@ -71,7 +75,11 @@
 extern "C" {
 #endif
 
-#define TC_ABI_VERSION 3
+#define TC_ABI_VERSION 4
+
+/* Segments at least this long are summed in pieces when a backward
+ * workspace covers them (tc_embed_backward). */
+#define TC_BACKWARD_SPLIT_PAIRS 2048
 
 typedef enum tc_status {
     TC_OK = 0,
@@ -169,12 +177,22 @@ tc_status tc_embed_expand(const float *grad_out, int32_t num_bags, int32_t dim,
  *   coal_grad[u, :] = sum over i in [seg_offsets[u], seg_offsets[u+1]), in
  *                     order, of expanded[sorted_pos[i], :], starting from +0,
  * with seg_offsets and sorted_pos from tc_argsort_rows. Equals
- * tc_embed_backward's coal_grad bit for bit (same rows, same order).
+ * tc_embed_backward's coal_grad bit for bit (same rows, same order), also
+ * with a workspace: workspace and workspace_bytes work as there.
  */
 tc_status tc_embed_coalesce(const float *expanded, int64_t num_pairs, int32_t dim,
                             const int32_t *seg_offsets, const int32_t *sorted_pos,
                             const int32_t *num_unique, int64_t max_unique, float *coal_grad,
-                            hipStream_t stream);
+                            void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Bytes of a backward workspace that covers a step of up to num_pairs pairs
+ * with rows of `dim` floats, for tc_embed_backward, tc_embed_backward_update
+ * and tc_embed_coalesce; 0 if no segment can be long (num_pairs < 128) or
+ * the arguments are out of range. About num_pairs * (dim / 256 + 0.15)
+ * bytes.
+ */
+size_t tc_backward_workspace_bytes(int64_t num_pairs, int32_t dim);
 
 /*
  * Casted gradient gather-reduce (Algorithm 3): for every u < *num_unique,
@@ -186,11 +204,28 @@ tc_status tc_embed_coalesce(const float *expanded, int64_t num_pairs, int32_t di
  *   max_unique capacity of coal_grad in rows (>= *num_unique), normally
  *              min(num_pairs, total_rows)
  *   coal_grad  [max_unique x dim] fp32; rows >= *num_unique are not written
+ *   workspace, workspace_bytes
+ *              optional (NULL, 0: none), sized with
+ *              tc_backward_workspace_bytes for the step's pairs. With it,
+ *              long segments are scheduled over persistent workgroups, and a
+ *              segment [b, b + len) with len >= TC_BACKWARD_SPLIT_PAIRS that
+ *              the workspace covers (b + len <= the num_pairs it was sized
+ *              for) is summed in pieces instead of one chain: n =
+ *              min(32, len / 1024) pieces, piece q being pairs
+ *              [b + floor(q*len/n), b + floor((q+1)*len/n)), each summed in
+ *              order from +0, and the n piece sums added in piece order from
+ *              +0. Other segments are summed as above. The order depends on
+ *              the segment's length only, so results still repeat bit for
+ *              bit. Device memory, 16-byte aligned (TC_ERR_INVALID_ARG
+ *              otherwise), read and written by the call; no initial contents
+ *              are needed and calls that share one workspace must not
+ *              overlap. Segments past the cover are still summed correctly,
+ *              as one chain, but slowly.
  */
 tc_status tc_embed_backward(const float *grad_out, int32_t num_bags, int32_t dim,
                             const int32_t *seg_offsets, const int32_t *casted_src,
                             const int32_t *num_unique, int64_t max_unique, float *coal_grad,
-                            hipStream_t stream);
+                            void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Gradient scatter + optimizer (Sec. II-B; RMSprop is Eq. 1, Adagrad Eq. 2).
@@ -231,7 +266,8 @@ tc_status tc_sparse_update(float *W, float *opt_state, int64_t total_rows, int32
  * applied to W[unique_rows[u]] (and the accumulator) exactly as
  * tc_sparse_update applies it. The results equal those two calls bit for
  * bit; the coalesced gradient is stored to coal_grad only if that is not
- * NULL. Arguments are those of the two calls (coal_grad optional); W,
+ * NULL. Arguments are those of the two calls (coal_grad optional, the
+ * workspace as for tc_embed_backward); W,
  * opt_state and grad_out must not overlap. Supports TC_OPT_SGD,
  * TC_OPT_ADAGRAD and TC_OPT_RMSPROP; TC_OPT_ROWWISE_ADAGRAD returns
  * TC_ERR_UNSUPPORTED (a row's columns are reduced by different workgroups,
@@ -243,7 +279,8 @@ tc_status tc_embed_backward_update(const float *grad_out, int32_t num_bags, int3
                                    const int32_t *unique_rows, const int32_t *num_unique,
                                    int64_t max_unique, float *W, float *opt_state,
                                    int64_t total_rows, int32_t opt_kind, float lr, float eps,
-                                   float gamma, float *coal_grad, hipStream_t stream);
+                                   float gamma, float *coal_grad, void *workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
 
 /* Static text for a status code. */
 const char *tc_status_string(tc_status status);

@@ -1,22 +1,32 @@
 // Backward: the casted gradient gather-reduce (Algorithm 3) on CDNA4.
 //
-// coal_grad[u] is the ordered sum of grad_out rows casted_src[j] over the
-// segment j in [seg_offsets[u], seg_offsets[u+1]). Segment lengths follow the
-// index skew: under Zipf lookups a few table rows own tens of thousands of
-// pairs, and each such sum is a dependency chain that must stay in order to
-// keep the result bitwise equal to the sequential definition. Two kernels
-// split the work by segment length:
+// coal_grad[u] is the sum of grad_out rows casted_src[j] over the segment j
+// in [seg_offsets[u], seg_offsets[u+1]). Segment lengths follow the index
+// skew: under Zipf lookups a few table rows own tens of thousands of pairs.
+// Segments under kLongSegment pairs are short; the others are long.
 //
-//  k_backward_long   segments of at least kLongSegment pairs. One workgroup
-//                    per (segment, 64-column part): four producer
-//                    wavefronts gather the rows into a ring of LDS buffers
-//                    with 16-byte loads, and one consumer wavefront (one
-//                    column per lane) runs the ordered adds out of LDS, so
-//                    the chain never waits behind load issue.
-//  k_backward_short  the other segments: lane groups exactly as the forward.
+//  k_backward_short  short segments: lane groups exactly as the forward.
+//  k_backward_long   long segments (no workspace): workgroups scan ranges of
+//                    segments for long ones.
+//  k_backward_list   long segments (workspace): persistent workgroups take
+//                    work items -- (long segment, part) or (piece of a split
+//                    segment, part) -- from lists the short kernel builds.
 //
-// The long kernel is launched first; both only read their inputs and write
-// disjoint rows of coal_grad. No atomics anywhere.
+// A long segment (or piece) is summed by one workgroup per 64-column part:
+// four producer wavefronts gather the rows into a ring of LDS buffers with
+// 16-byte loads, and one consumer wavefront (one column per lane) runs the
+// ordered adds out of LDS, so the chain never waits behind load issue.
+//
+// Summation order. Without a workspace every segment is one ordered chain
+// from +0, the sequential definition bit for bit. With a workspace that
+// covers them, segments of kSplitPairs pairs or more are cut into n =
+// min(kMaxPieces, len / kPieceMin) pieces of consecutive pairs; each piece is
+// an ordered chain from +0 run by its own work item, which stores the piece
+// sum, and the item that finishes a segment's last piece (an agent-scope
+// counter per segment and part) adds the n piece sums in piece order from
+// +0. The order is fixed by the segment's length alone, so results do not
+// depend on scheduling and repeat bit for bit; the chain of the hottest row
+// shrinks from len to len / n.
 //
 // Fused with the update (tc_embed_backward_update), the owner of coalesced
 // row u applies the optimizer step to table row unique_rows[u] straight from
@@ -31,7 +41,7 @@
 namespace tc {
 namespace {
 
-// Segments at least this long go to k_backward_long.
+// Segments at least this long are long.
 constexpr int kLongSegment = 128;
 // A long-segment workgroup: one consumer and kProducers producer wavefronts.
 constexpr int kProducers = 4;
@@ -55,6 +65,43 @@ static_assert(kPeriod % kAhead == 0 && kPeriod % kIdAhead == 0 && kPeriod % kBuf
               "ring periods must divide kPeriod");
 // Ranges of segments scanned by the blocks of the long kernel (per part).
 constexpr int kLongRanges = 1024;
+// Summing in pieces (with a workspace): segments of at least kSplitPairs
+// pairs, pieces of at least kPieceMin pairs, at most kMaxPieces of them.
+constexpr int32_t kSplitPairs = TC_BACKWARD_SPLIT_PAIRS;
+constexpr int32_t kPieceMin = 1024;
+constexpr int32_t kMaxPieces = 32;
+static_assert(kSplitPairs >= 2 * kPieceMin && kPieceMin >= kLongSegment, "piece sizes");
+
+// The backward workspace. The lists are filled by k_backward_short and
+// drained by k_backward_list; k_backward_init zeroes the counters first.
+// A long segment [beg, beg + len) is covered when beg + len <= cap_pairs and
+// split when also len >= kSplitPairs. Split segments are disjoint intervals
+// of at least kSplitPairs pairs, and pieces of at least kPieceMin pairs, so
+// beg / kSplitPairs and (first pair of the piece) / kPieceMin name them
+// without collisions.
+//   ctr[0], ctr[1]   entries in pieces[] and longs[]; ctr[2] next work item
+//   pieces[k]        {u, beg, len, q}: piece q of split segment u
+//   longs[k]         {u, beg, len, 0}: a covered long segment, not split
+//   seg_done[(beg / kSplitPairs) * parts + p]  pieces of part p finished
+//   partial[(first pair / kPieceMin) * dim + c]  piece sums
+struct SplitWs {
+    int32_t *ctr;
+    int4 *pieces;
+    int4 *longs;
+    int32_t *seg_done;
+    float *partial;
+    int64_t cap_pairs;  // 0: no workspace
+    int32_t max_pieces, max_longs;
+    int32_t parts;
+};
+
+__device__ __forceinline__ int32_t num_pieces(int32_t len) {
+    return len / kPieceMin < kMaxPieces ? len / kPieceMin : kMaxPieces;
+}
+__device__ __forceinline__ int32_t piece_begin(int32_t beg, int32_t len, int32_t n, int32_t q) {
+    return beg + int32_t(int64_t(q) * len / n);
+}
+
 // Buffer resource word 3 for gfx9-family buffers; out-of-range reads give 0.
 constexpr int32_t kBufferWord3 = 0x00020000;
 // A buffer offset past every resource here (resources span < 2^31 bytes):
@@ -62,11 +109,6 @@ constexpr int32_t kBufferWord3 = 0x00020000;
 // (a sum started at +0.0 is never -0.0, and x + 0.0 == x for every other x).
 constexpr int32_t kOutOfRange = 0x7ffff000;
 
-// LDS buffer layout: column-major, so that one 16-byte read gives a consumer
-// lane four consecutive rows of its column. Within column c, the group of
-// rows 4k..4k+3 sits at group position k ^ swz(c); the swizzle spreads both
-// the consumer's 16-byte reads (16 neighbouring columns, same k) and the
-// producers' 4-byte writes (16 columns 4 apart, same k) over distinct banks.
 // What becomes of a coalesced row: stored to coal (if not null) and/or
 // applied to W[rows[u]] (if W is not null) with optimizer `kind`.
 struct RowSink {
@@ -140,6 +182,11 @@ __device__ __forceinline__ void sink_group(const RowSink &k, int64_t u, int32_t 
     }
 }
 
+// LDS buffer layout: column-major, so that one 16-byte read gives a consumer
+// lane four consecutive rows of its column. Within column c, the group of
+// rows 4k..4k+3 sits at group position k ^ swz(c); the swizzle spreads both
+// the consumer's 16-byte reads (16 neighbouring columns, same k) and the
+// producers' 4-byte writes (16 columns 4 apart, same k) over distinct banks.
 struct LongLds {
     alignas(16) float cols[kBuffers][kPartCols][kChunkRows];
     int32_t offs[kProducers][kChunkRows];
@@ -310,11 +357,79 @@ __device__ float long_consumer(LongLds &lds, int32_t nchunks) {
     return acc;
 }
 
-// Each block (range x, part y) scans a contiguous range of segments and runs
-// every long one it finds for its part. All four wavefronts scan the same
-// offsets, so they agree on every segment and on its number of chunks, which
-// fixes the barrier count. A first pass reads every 64th offset: a batch of
-// 64 segments spanning fewer than kLongSegment pairs cannot hold a long one.
+// The ordered chain over ids[beg, beg + len) for this block's part, run by
+// all five wavefronts (each executes the same number of barriers). Returns
+// the sum of column `col` in the consumer wavefront (w == 0), 0 elsewhere.
+__device__ __forceinline__ float run_chain(LongLds &lds, const float *__restrict__ grad,
+                                           int32_t dim, const int32_t *__restrict__ ids,
+                                           int32_t beg, int32_t len, int w, int32_t part,
+                                           int32_t col) {
+    const int32_t row_bytes = dim * 4;
+    const int32_t *sid = ids + beg;
+    // ids within a segment are non-decreasing (stable cast order)
+    const int32_t first = __builtin_amdgcn_readfirstlane(sid[0]);
+    const int32_t last = __builtin_amdgcn_readfirstlane(sid[len - 1]);
+    const uint64_t span = uint64_t(last - first + 1) * uint64_t(row_bytes);
+    if (span >= (uint64_t(1) << 31) || len >= (1 << 29)) {
+        // rows spread over 2 GiB or more (or a segment too long for 32-bit
+        // byte offsets of its ids): the consumer alone, with 64-bit addressed
+        // loads (no barriers on this path)
+        float acc = 0.f;
+        if (w == 0) {
+            const float *colp = grad + (col < dim ? col : dim - 1);
+            for (int32_t k = 0; k < len; ++k) acc = acc + colp[int64_t(sid[k]) * dim];
+        }
+        return acc;
+    }
+    const int32_t nchunks = (len + kChunkRows - 1) / kChunkRows;
+    const auto id_rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t *>(sid), 0, len * 4, kBufferWord3);
+    const auto rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float *>(grad + int64_t(first) * dim), 0, int32_t(span), kBufferWord3);
+    const int32_t part_bytes = part * kPartCols * 4;
+    if (w == 0) return long_consumer(lds, nchunks);
+    if (w == 1)
+        long_producer<0>(lds, id_rsrc, len, first, row_bytes, part_bytes, nchunks, rsrc);
+    else if (w == 2)
+        long_producer<1>(lds, id_rsrc, len, first, row_bytes, part_bytes, nchunks, rsrc);
+    else if (w == 3)
+        long_producer<2>(lds, id_rsrc, len, first, row_bytes, part_bytes, nchunks, rsrc);
+    else
+        long_producer<3>(lds, id_rsrc, len, first, row_bytes, part_bytes, nchunks, rsrc);
+    return 0.f;
+}
+
+// Consumer wavefront, after piece q of split segment u: store the piece sum,
+// count the piece, and if it was the segment's last (for this part), add the
+// n piece sums in piece order from +0 and hand the row to the sink.
+__device__ void finish_piece(const SplitWs &ws, const RowSink &sink, int32_t dim, int32_t part,
+                             int32_t col, int32_t u, int32_t beg, int32_t len, int32_t n,
+                             int32_t q, float acc) {
+    const int lane = threadIdx.x & (kWave - 1);
+    if (col < dim)
+        ws.partial[int64_t(piece_begin(beg, len, n, q) / kPieceMin) * dim + col] = acc;
+    // the piece sum reaches device scope before the count does
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    int32_t done = 0;
+    if (lane == 0)
+        done = __hip_atomic_fetch_add(&ws.seg_done[int64_t(beg / kSplitPairs) * ws.parts + part],
+                                      1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    done = __builtin_amdgcn_readlane(done, 0);
+    if (done != n - 1) return;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    if (col >= dim) return;
+    float tot = 0.f;
+    for (int32_t k = 0; k < n; ++k)
+        tot = tot + ws.partial[int64_t(piece_begin(beg, len, n, k) / kPieceMin) * dim + col];
+    sink_value(sink, u, dim, col, tot);
+}
+
+// Long segments without a workspace. Each block (range x, part y) scans a
+// contiguous range of segments and runs every long one it finds. All five
+// wavefronts scan the same offsets, so they agree on every segment and on its
+// number of chunks, which fixes the barrier count. A first pass reads every
+// 64th offset: a batch of 64 segments spanning fewer than kLongSegment pairs
+// cannot hold a long one.
 __global__ __launch_bounds__(kLongThreads) void k_backward_long(
     const float *__restrict__ grad, int32_t dim, const int32_t *__restrict__ ids,
     const int32_t *__restrict__ offsets, const int32_t *__restrict__ num_out_dev,
@@ -324,13 +439,14 @@ __global__ __launch_bounds__(kLongThreads) void k_backward_long(
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int32_t part = blockIdx.y;
     const int32_t col = part * kPartCols + lane;
-    const int32_t row_bytes = dim * 4;
     const int64_t u_dev = *num_out_dev;
     const int64_t num = u_dev < num_out_cap ? u_dev : num_out_cap;
-    const int64_t per = (num + gridDim.x - 1) / gridDim.x;
-    const int64_t r0 = int64_t(blockIdx.x) * per;
-    const int64_t r1 = r0 + per < num ? r0 + per : num;
     if (w == 0) __builtin_amdgcn_s_setprio(3);
+    const int32_t ranges = int32_t(gridDim.x);
+    const int32_t range = int32_t(blockIdx.x);
+    const int64_t per = (num + ranges - 1) / ranges;
+    const int64_t r0 = int64_t(range) * per;
+    const int64_t r1 = r0 + per < num ? r0 + per : num;
     for (int64_t c0 = r0; c0 < r1; c0 += int64_t(kWave) * kWave) {
         const int64_t s0 = c0 + int64_t(kWave) * lane;  // this lane's batch
         const int32_t os = offsets[s0 < r1 ? s0 : r1];
@@ -353,46 +469,64 @@ __global__ __launch_bounds__(kLongThreads) void k_backward_long(
                 const int32_t beg = __builtin_amdgcn_readlane(o0, j);
                 const int32_t len = __builtin_amdgcn_readlane(o1, j) - beg;
                 const int64_t seg = c0 + int64_t(kWave) * i + j;
-                const int32_t *sid = ids + beg;
-                // ids within a segment are non-decreasing (stable cast order)
-                const int32_t first = __builtin_amdgcn_readfirstlane(sid[0]);
-                const int32_t last = __builtin_amdgcn_readfirstlane(sid[len - 1]);
-                const uint64_t span = uint64_t(last - first + 1) * uint64_t(row_bytes);
-                if (span >= (uint64_t(1) << 31) || len >= (1 << 29)) {
-                    // rows spread over 2 GiB or more (or a segment too long for
-                    // 32-bit byte offsets of its ids): the consumer alone, with
-                    // 64-bit addressed loads (no barriers on this path)
-                    if (w == 0) {
-                        float acc = 0.f;
-                        const float *colp = grad + (col < dim ? col : dim - 1);
-                        for (int32_t k = 0; k < len; ++k)
-                            acc = acc + colp[int64_t(sid[k]) * dim];
-                        if (col < dim) sink_value(sink, seg, dim, col, acc);
-                    }
-                    continue;
-                }
-                const int32_t nchunks = (len + kChunkRows - 1) / kChunkRows;
-                const auto id_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-                    const_cast<int32_t *>(sid), 0, len * 4, kBufferWord3);
-                const auto rsrc = __builtin_amdgcn_make_buffer_rsrc(
-                    const_cast<float *>(grad + int64_t(first) * dim), 0, int32_t(span),
-                    kBufferWord3);
-                const int32_t part_bytes = part * kPartCols * 4;
-                if (w == 0) {
-                    const float acc = long_consumer(lds, nchunks);
-                    if (col < dim) sink_value(sink, seg, dim, col, acc);
-                } else if (w == 1) {
-                    long_producer<0>(lds, id_rsrc, len, first, row_bytes, part_bytes, nchunks, rsrc);
-                } else if (w == 2) {
-                    long_producer<1>(lds, id_rsrc, len, first, row_bytes, part_bytes, nchunks, rsrc);
-                } else if (w == 3) {
-                    long_producer<2>(lds, id_rsrc, len, first, row_bytes, part_bytes, nchunks, rsrc);
-                } else {
-                    long_producer<3>(lds, id_rsrc, len, first, row_bytes, part_bytes, nchunks, rsrc);
-                }
+                const float acc = run_chain(lds, grad, dim, ids, beg, len, w, part, col);
+                if (w == 0 && col < dim) sink_value(sink, seg, dim, col, acc);
             }
         }
     }
+}
+
+// Long segments with a workspace: persistent blocks take work items
+// (index / parts = list entry, pieces first; index % parts = part) from an
+// agent-scope counter until the lists are drained. The next item is fetched
+// while the current one runs.
+__global__ __launch_bounds__(kLongThreads, 3) void k_backward_list(
+    const float *__restrict__ grad, int32_t dim, const int32_t *__restrict__ ids, RowSink sink,
+    SplitWs ws) {
+    __shared__ LongLds lds;
+    __shared__ int32_t next_item;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int32_t np = min(ws.ctr[0], ws.max_pieces);
+    const int32_t nl = min(ws.ctr[1], ws.max_longs);
+    const int64_t total = int64_t(np + nl) * ws.parts;
+    if (threadIdx.x == 0)
+        next_item = __hip_atomic_fetch_add(&ws.ctr[2], 1, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+    lds_barrier();
+    int32_t item = next_item;
+    if (w == 0) __builtin_amdgcn_s_setprio(3);
+    while (item < total) {
+        int32_t ahead = 0;
+        if (threadIdx.x == 0)
+            ahead = __hip_atomic_fetch_add(&ws.ctr[2], 1, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+        const int32_t k = item / ws.parts, part = item % ws.parts;
+        const int32_t col = part * kPartCols + lane;
+        const int4 e = k < np ? ws.pieces[k] : ws.longs[k - np];
+        const int32_t u = __builtin_amdgcn_readfirstlane(e.x);
+        const int32_t beg = __builtin_amdgcn_readfirstlane(e.y);
+        const int32_t len = __builtin_amdgcn_readfirstlane(e.z);
+        if (k < np) {
+            const int32_t q = __builtin_amdgcn_readfirstlane(e.w);
+            const int32_t n = num_pieces(len);
+            const int32_t p0 = piece_begin(beg, len, n, q);
+            const int32_t p1 = piece_begin(beg, len, n, q + 1);
+            const float acc = run_chain(lds, grad, dim, ids, p0, p1 - p0, w, part, col);
+            if (w == 0) finish_piece(ws, sink, dim, part, col, u, beg, len, n, q, acc);
+        } else {
+            const float acc = run_chain(lds, grad, dim, ids, beg, len, w, part, col);
+            if (w == 0 && col < dim) sink_value(sink, u, dim, col, acc);
+        }
+        lds_barrier();  // every wavefront is past this item
+        if (threadIdx.x == 0) next_item = ahead;
+        lds_barrier();
+        item = next_item;
+    }
+}
+
+__global__ void k_backward_init(SplitWs ws) {
+    if (threadIdx.x < 3) ws.ctr[threadIdx.x] = 0;
 }
 
 // Short segments: one lane group per segment, as the forward; long ones are
@@ -401,7 +535,7 @@ template <int LANES, int CHUNKS>
 __global__ __launch_bounds__(kBlock) void k_backward_short(
     const float *__restrict__ grad, int32_t dim, const int32_t *__restrict__ ids,
     const int32_t *__restrict__ offsets, const int32_t *__restrict__ num_out_dev,
-    int64_t num_out_cap, RowSink sink) {
+    int64_t num_out_cap, RowSink sink, SplitWs ws) {
     constexpr int kGroups = kWave / LANES;
     const int lane = threadIdx.x & (kWave - 1);
     const int sub = lane & (LANES - 1);
@@ -414,11 +548,42 @@ __global__ __launch_bounds__(kBlock) void k_backward_short(
         const int64_t o = o0 + grp;
         int32_t beg = 0, end = 0;
         bool mine = false;
+        bool listed = false;  // a covered long segment, not split
+        int32_t len = 0;
         if (o < num) {
             beg = offsets[o];
             end = offsets[o + 1];
-            mine = end - beg < kLongSegment;
+            len = end - beg;
+            const bool covered = len >= kLongSegment && int64_t(beg) + len <= ws.cap_pairs;
+            // without a workspace long segments go to k_backward_long; with
+            // one, covered ones go to the lists and uncovered ones stay here
+            mine = ws.cap_pairs == 0 ? len < kLongSegment : !covered;
+            if (covered && len >= kSplitPairs) {
+                if (sub == 0) {
+                    const int32_t n = num_pieces(len);
+                    const int32_t at = __hip_atomic_fetch_add(
+                        &ws.ctr[0], n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    for (int32_t q = 0; q < n && at + q < ws.max_pieces; ++q)
+                        ws.pieces[at + q] = make_int4(int32_t(o), beg, len, q);
+                    const int64_t slot = beg / kSplitPairs;
+                    for (int32_t p = 0; p < ws.parts; ++p) ws.seg_done[slot * ws.parts + p] = 0;
+                }
+            } else {
+                listed = covered && sub == 0;
+            }
             if (!mine) end = beg;
+        }
+        // one counter update per wavefront for the long-segment list
+        const uint64_t lm = __ballot(listed);
+        if (lm) {
+            const int leader = __builtin_ctzll(lm);
+            int32_t at = 0;
+            if (lane == leader)
+                at = __hip_atomic_fetch_add(&ws.ctr[1], __builtin_popcountll(lm), __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT);
+            at = __builtin_amdgcn_readlane(at, leader) +
+                 __builtin_popcountll(lm & ((uint64_t(1) << lane) - 1));
+            if (listed && at < ws.max_longs) ws.longs[at] = make_int4(int32_t(o), beg, len, 0);
         }
         float4 acc[CHUNKS];
 #pragma unroll
@@ -485,23 +650,85 @@ tc_status launch_expand(const float *grad, int32_t dim, const int32_t *bag_offse
     return TC_ERR_UNSUPPORTED;
 }
 
+// The backward workspace's layout for a cover of cap pairs.
+struct WsLayout {
+    size_t ctr, pieces, longs, seg_done, partial, total;
+    int32_t max_pieces, max_longs;
+};
+WsLayout ws_layout(int64_t cap, int32_t dim) {
+    auto al = [](int64_t x) { return size_t((x + 255) & ~int64_t(255)); };
+    const int64_t parts = (dim + kPartCols - 1) / kPartCols;
+    WsLayout l;
+    l.max_pieces = int32_t(cap / kPieceMin + 1);
+    l.max_longs = int32_t(cap / kLongSegment + 1);
+    l.ctr = 0;
+    l.pieces = l.ctr + al(4 * 4);
+    l.longs = l.pieces + al(int64_t(l.max_pieces) * 16);
+    l.seg_done = l.longs + al(int64_t(l.max_longs) * 16);
+    l.partial = l.seg_done + al((cap / kSplitPairs + 1) * parts * 4);
+    l.total = l.partial + al(int64_t(l.max_pieces) * dim * 4);
+    return l;
+}
+
+// The workspace in `bytes` at `ws`: it covers the largest cap (below 2^31)
+// whose layout fits; cap 0 (no workspace) if ws is null or not even
+// kLongSegment pairs fit.
+SplitWs make_split_ws(void *ws, size_t bytes, int32_t dim) {
+    SplitWs s{nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0, 0,
+              (dim + kPartCols - 1) / kPartCols};
+    if (ws == nullptr || ws_layout(kLongSegment, dim).total > bytes) return s;
+    int64_t lo = kLongSegment, hi = (int64_t(1) << 31) - 1;
+    while (lo < hi) {  // largest cap whose layout fits
+        const int64_t mid = lo + (hi - lo + 1) / 2;
+        if (ws_layout(mid, dim).total <= bytes) lo = mid; else hi = mid - 1;
+    }
+    const WsLayout l = ws_layout(lo, dim);
+    char *p = static_cast<char *>(ws);
+    s.ctr = reinterpret_cast<int32_t *>(p + l.ctr);
+    s.pieces = reinterpret_cast<int4 *>(p + l.pieces);
+    s.longs = reinterpret_cast<int4 *>(p + l.longs);
+    s.seg_done = reinterpret_cast<int32_t *>(p + l.seg_done);
+    s.partial = reinterpret_cast<float *>(p + l.partial);
+    s.cap_pairs = lo;
+    s.max_pieces = l.max_pieces;
+    s.max_longs = l.max_longs;
+    return s;
+}
+
+// Workgroups of k_backward_list: as many as can be resident at once.
+int list_blocks() {
+    static int blocks = 0;
+    if (blocks == 0) {
+        int per_cu = 0, cus = 0, dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_backward_list, kLongThreads,
+                                                         0) != hipSuccess ||
+            per_cu < 1 || cus < 1)
+            return kNumCUs;
+        blocks = per_cu * cus;
+    }
+    return blocks;
+}
+
 tc_status launch_backward(const float *grad, int32_t dim, const int32_t *ids,
                           const int32_t *offsets, const int32_t *num_out_dev, int64_t cap,
-                          const RowSink &out, hipStream_t stream) {
-    const int parts = (dim + kPartCols - 1) / kPartCols;
-    const int ranges = kLongRanges / parts > 64 ? kLongRanges / parts : 64;
-    k_backward_long<<<dim3(ranges, parts), kLongThreads, 0, stream>>>(grad, dim, ids, offsets,
-                                                                       num_out_dev, cap, out);
-    tc_status st = check_launch("k_backward_long");
-    if (st != TC_OK) return st;
+                          const RowSink &out, const SplitWs &ws, hipStream_t stream) {
+    if (ws.cap_pairs > 0) {
+        k_backward_init<<<1, kWave, 0, stream>>>(ws);
+        const tc_status st = check_launch("k_backward_init");
+        if (st != TC_OK) return st;
+    }
+    // the short kernel first: it builds the lists
     const RowShape s = row_shape(dim);
     const int64_t rows_per_block = (kBlock / kWave) * (kWave / s.lanes);
     const unsigned grid = grid_for(cap, rows_per_block, int64_t(kNumCUs) * 8);
+    bool launched = false;
 #define TC_BWD_CASE(L, C)                                                                    \
-    if (s.lanes == L && s.chunks == C) {                                                     \
+    if (!launched && s.lanes == L && s.chunks == C) {                                        \
         k_backward_short<L, C><<<grid, kBlock, 0, stream>>>(grad, dim, ids, offsets,          \
-                                                            num_out_dev, cap, out);          \
-        return check_launch("k_backward_short");                                             \
+                                                            num_out_dev, cap, out, ws);      \
+        launched = true;                                                                     \
     }
     TC_BWD_CASE(1, 1)
     TC_BWD_CASE(2, 1)
@@ -514,8 +741,21 @@ tc_status launch_backward(const float *grad, int32_t dim, const int32_t *ids,
     TC_BWD_CASE(64, 3)
     TC_BWD_CASE(64, 4)
 #undef TC_BWD_CASE
-    set_error("no backward kernel for dim %d", dim);
-    return TC_ERR_UNSUPPORTED;
+    if (!launched) {
+        set_error("no backward kernel for dim %d", dim);
+        return TC_ERR_UNSUPPORTED;
+    }
+    tc_status st = check_launch("k_backward_short");
+    if (st != TC_OK) return st;
+    if (ws.cap_pairs > 0) {
+        k_backward_list<<<list_blocks(), kLongThreads, 0, stream>>>(grad, dim, ids, out, ws);
+        return check_launch("k_backward_list");
+    }
+    const int parts = (dim + kPartCols - 1) / kPartCols;
+    const int ranges = kLongRanges / parts > 64 ? kLongRanges / parts : 64;
+    k_backward_long<<<dim3(ranges, parts), kLongThreads, 0, stream>>>(grad, dim, ids, offsets,
+                                                                       num_out_dev, cap, out);
+    return check_launch("k_backward_long");
 }
 
 }  // namespace
@@ -526,7 +766,8 @@ using namespace tc;
 extern "C" tc_status tc_embed_backward(const float *grad_out, int32_t num_bags, int32_t dim,
                                        const int32_t *seg_offsets, const int32_t *casted_src,
                                        const int32_t *num_unique, int64_t max_unique,
-                                       float *coal_grad, hipStream_t stream) {
+                                       float *coal_grad, void *workspace,
+                                       size_t workspace_bytes, hipStream_t stream) {
     clear_error();
     TC_REQUIRE(num_bags >= 0 && max_unique >= 0, TC_ERR_INVALID_ARG,
                "tc_embed_backward: negative size");
@@ -539,16 +780,19 @@ extern "C" tc_status tc_embed_backward(const float *grad_out, int32_t num_bags, 
                TC_ERR_INVALID_ARG, "tc_embed_backward: null pointer");
     TC_REQUIRE(aligned16(grad_out) && aligned16(coal_grad), TC_ERR_UNSUPPORTED,
                "tc_embed_backward: grad_out and coal_grad must be 16-byte aligned");
+    TC_REQUIRE(workspace_bytes == 0 || (workspace && aligned16(workspace)), TC_ERR_INVALID_ARG,
+               "tc_embed_backward: workspace must be a 16-byte aligned pointer");
     const RowSink sink{coal_grad, nullptr, nullptr, nullptr, TC_OPT_SGD, 0.f, 0.f, 0.f, 1.f};
     return launch_backward(grad_out, dim, casted_src, seg_offsets, num_unique, max_unique, sink,
-                           stream);
+                           make_split_ws(workspace, workspace_bytes, dim), stream);
 }
 
 extern "C" tc_status tc_embed_backward_update(
     const float *grad_out, int32_t num_bags, int32_t dim, const int32_t *seg_offsets,
     const int32_t *casted_src, const int32_t *unique_rows, const int32_t *num_unique,
     int64_t max_unique, float *W, float *opt_state, int64_t total_rows, int32_t opt_kind,
-    float lr, float eps, float gamma, float *coal_grad, hipStream_t stream) {
+    float lr, float eps, float gamma, float *coal_grad, void *workspace, size_t workspace_bytes,
+    hipStream_t stream) {
     clear_error();
     TC_REQUIRE(num_bags >= 0 && max_unique >= 0 && total_rows >= 0, TC_ERR_INVALID_ARG,
                "tc_embed_backward_update: negative size");
@@ -573,10 +817,12 @@ extern "C" tc_status tc_embed_backward_update(
                    (!coal_grad || aligned16(coal_grad)),
                TC_ERR_UNSUPPORTED,
                "tc_embed_backward_update: float pointers must be 16-byte aligned");
+    TC_REQUIRE(workspace_bytes == 0 || (workspace && aligned16(workspace)), TC_ERR_INVALID_ARG,
+               "tc_embed_backward_update: workspace must be a 16-byte aligned pointer");
     const RowSink sink{coal_grad, W, opt_state, unique_rows, opt_kind, lr, eps, gamma,
                        1.0f - gamma};
     return launch_backward(grad_out, dim, casted_src, seg_offsets, num_unique, max_unique, sink,
-                           stream);
+                           make_split_ws(workspace, workspace_bytes, dim), stream);
 }
 
 extern "C" tc_status tc_embed_expand(const float *grad_out, int32_t num_bags, int32_t dim,
@@ -600,7 +846,8 @@ extern "C" tc_status tc_embed_expand(const float *grad_out, int32_t num_bags, in
 extern "C" tc_status tc_embed_coalesce(const float *expanded, int64_t num_pairs, int32_t dim,
                                        const int32_t *seg_offsets, const int32_t *sorted_pos,
                                        const int32_t *num_unique, int64_t max_unique,
-                                       float *coal_grad, hipStream_t stream) {
+                                       float *coal_grad, void *workspace,
+                                       size_t workspace_bytes, hipStream_t stream) {
     clear_error();
     TC_REQUIRE(num_pairs >= 0 && max_unique >= 0, TC_ERR_INVALID_ARG,
                "tc_embed_coalesce: negative size");
@@ -613,9 +860,18 @@ extern "C" tc_status tc_embed_coalesce(const float *expanded, int64_t num_pairs,
                TC_ERR_INVALID_ARG, "tc_embed_coalesce: null pointer");
     TC_REQUIRE(aligned16(expanded) && aligned16(coal_grad), TC_ERR_UNSUPPORTED,
                "tc_embed_coalesce: expanded and coal_grad must be 16-byte aligned");
+    TC_REQUIRE(workspace_bytes == 0 || (workspace && aligned16(workspace)), TC_ERR_INVALID_ARG,
+               "tc_embed_coalesce: workspace must be a 16-byte aligned pointer");
     // Algorithm 1's accumulate is the casted gather-reduce over the expanded
     // rows, in sorted order: the same kernels with sorted positions as ids.
     const RowSink sink{coal_grad, nullptr, nullptr, nullptr, TC_OPT_SGD, 0.f, 0.f, 0.f, 1.f};
     return launch_backward(expanded, dim, sorted_pos, seg_offsets, num_unique, max_unique, sink,
-                           stream);
+                           make_split_ws(workspace, workspace_bytes, dim), stream);
+}
+
+extern "C" size_t tc_backward_workspace_bytes(int64_t num_pairs, int32_t dim) {
+    if (num_pairs < kLongSegment || dim <= 0 || dim > kMaxDim ||
+        num_pairs >= (int64_t(1) << 31))
+        return 0;
+    return ws_layout(num_pairs, dim).total;
 }

@@ -27,15 +27,16 @@ _SIGNATURES = {
     "tc_cast_workspace_bytes": (_sz, [_i64, _i64, _i32]),
     "tc_cast_index": (_i32, [_vp, _i32, _i32, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp,
                              _vp, _vp, _sz, _vp]),
-    "tc_embed_backward": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _i64, _vp, _vp]),
+    "tc_embed_backward": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _i64, _vp, _vp, _sz, _vp]),
+    "tc_backward_workspace_bytes": (_sz, [_i64, _i32]),
     "tc_sparse_update": (_i32, [_vp, _vp, _i64, _i32, _vp, _vp, _vp, _i64, _i32, _f32, _f32,
                                 _f32, _vp]),
     "tc_embed_backward_update": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _vp,
-                                        _i64, _i32, _f32, _f32, _f32, _vp, _vp]),
+                                        _i64, _i32, _f32, _f32, _f32, _vp, _vp, _sz, _vp]),
     "tc_argsort_rows": (_i32, [_vp, _i32, _i32, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp,
                                _vp, _sz, _vp]),
     "tc_embed_expand": (_i32, [_vp, _i32, _i32, _vp, _i64, _vp, _vp]),
-    "tc_embed_coalesce": (_i32, [_vp, _i64, _i32, _vp, _vp, _vp, _i64, _vp, _vp]),
+    "tc_embed_coalesce": (_i32, [_vp, _i64, _i32, _vp, _vp, _vp, _i64, _vp, _vp, _sz, _vp]),
     "tc_status_string": (ctypes.c_char_p, [_i32]),
     "tc_last_error": (ctypes.c_char_p, []),
     "tc_abi_version": (_i32, []),
@@ -118,13 +119,23 @@ def tc_cast_index(table_row_offset, num_tables, bags_per_table, total_rows, max_
         _stream(stream)), "tc_cast_index")
 
 
+def _ws(workspace):
+    return (_ptr(workspace, None, "workspace"),
+            0 if workspace is None else workspace.numel() * workspace.element_size())
+
+
+def tc_backward_workspace_bytes(num_pairs: int, dim: int) -> int:
+    return int(_lib.tc_backward_workspace_bytes(num_pairs, dim))
+
+
 def tc_embed_backward(grad_out, seg_offsets, casted_src, num_unique, max_unique, coal_grad,
-                      stream=None) -> None:
+                      workspace=None, stream=None) -> None:
     _check(_lib.tc_embed_backward(
         _ptr(grad_out, torch.float32, "grad_out"), grad_out.shape[0], grad_out.shape[1],
         _ptr(seg_offsets, torch.int32, "seg_offsets"), _ptr(casted_src, torch.int32, "casted_src"),
         _ptr(num_unique, torch.int32, "num_unique"), max_unique,
-        _ptr(coal_grad, torch.float32, "coal_grad"), _stream(stream)), "tc_embed_backward")
+        _ptr(coal_grad, torch.float32, "coal_grad"), *_ws(workspace), _stream(stream)),
+        "tc_embed_backward")
 
 
 def tc_sparse_update(W, opt_state, unique_rows, coal_grad, num_unique, max_unique, opt_kind, lr,
@@ -138,14 +149,14 @@ def tc_sparse_update(W, opt_state, unique_rows, coal_grad, num_unique, max_uniqu
 
 def tc_embed_backward_update(grad_out, seg_offsets, casted_src, unique_rows, num_unique,
                              max_unique, W, opt_state, opt_kind, lr, eps, gamma=0.0,
-                             coal_grad=None, stream=None) -> None:
+                             coal_grad=None, workspace=None, stream=None) -> None:
     _check(_lib.tc_embed_backward_update(
         _ptr(grad_out, torch.float32, "grad_out"), grad_out.shape[0], grad_out.shape[1],
         _ptr(seg_offsets, torch.int32, "seg_offsets"), _ptr(casted_src, torch.int32, "casted_src"),
         _ptr(unique_rows, torch.int32, "unique_rows"), _ptr(num_unique, torch.int32, "num_unique"),
         max_unique, _ptr(W, torch.float32, "W"), _ptr(opt_state, torch.float32, "opt_state"),
         W.shape[0], opt_kind, lr, eps, gamma, _ptr(coal_grad, torch.float32, "coal_grad"),
-        _stream(stream)), "tc_embed_backward_update")
+        *_ws(workspace), _stream(stream)), "tc_embed_backward_update")
 
 
 def tc_argsort_rows(table_row_offset, num_tables, bags_per_table, total_rows, max_table_rows,
@@ -170,12 +181,13 @@ def tc_embed_expand(grad_out, bag_offsets, num_pairs, expanded, stream=None) -> 
 
 
 def tc_embed_coalesce(expanded, num_pairs, seg_offsets, sorted_pos, num_unique, max_unique,
-                      coal_grad, stream=None) -> None:
+                      coal_grad, workspace=None, stream=None) -> None:
     _check(_lib.tc_embed_coalesce(
         _ptr(expanded, torch.float32, "expanded"), num_pairs, expanded.shape[1],
         _ptr(seg_offsets, torch.int32, "seg_offsets"), _ptr(sorted_pos, torch.int32, "sorted_pos"),
         _ptr(num_unique, torch.int32, "num_unique"), max_unique,
-        _ptr(coal_grad, torch.float32, "coal_grad"), _stream(stream)), "tc_embed_coalesce")
+        _ptr(coal_grad, torch.float32, "coal_grad"), *_ws(workspace), _stream(stream)),
+        "tc_embed_coalesce")
 
 
 class EmbeddingTrainer:
@@ -187,7 +199,11 @@ class EmbeddingTrainer:
 
     def __init__(self, *, total_rows: int, dim: int, num_tables: int, bags_per_table: int,
                  max_pairs: int, optimizer: str = "sgd", lr: float = 0.01, eps: float = 1e-8,
-                 gamma: float = 0.99, device="cuda", table: torch.Tensor | None = None, max_table_rows: int = 0):
+                 gamma: float = 0.99, device="cuda", table: torch.Tensor | None = None,
+                 max_table_rows: int = 0, split_long: bool = True):
+        """split_long: give the backward a workspace, so that segments of
+        TC_BACKWARD_SPLIT_PAIRS pairs or more are summed in pieces (faster
+        under skew; without it every segment is one ordered chain)."""
         self.total_rows, self.dim = total_rows, dim
         self.num_tables, self.bags_per_table = num_tables, bags_per_table
         self.num_bags = num_tables * bags_per_table
@@ -214,6 +230,9 @@ class EmbeddingTrainer:
         self.coal = torch.empty((max(self.max_unique, 1), dim), dtype=torch.float32, device=device)
         ws = tc_cast_workspace_bytes(max_pairs, total_rows, num_tables)
         self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=device)
+        bws = tc_backward_workspace_bytes(max_pairs, dim) if split_long else 0
+        self.bwd_workspace = (torch.empty(bws, dtype=torch.uint8, device=device) if bws
+                              else None)
 
     def forward(self, table_row_offset, indices, bag_offsets, stream=None):
         tc_embed_forward(self.W, table_row_offset, self.num_tables, self.bags_per_table, indices,
@@ -228,7 +247,7 @@ class EmbeddingTrainer:
 
     def backward(self, grad_out, stream=None):
         tc_embed_backward(grad_out, self.seg_offsets, self.casted_src, self.num_unique,
-                          self.max_unique, self.coal, stream)
+                          self.max_unique, self.coal, self.bwd_workspace, stream)
 
     def update(self, stream=None):
         tc_sparse_update(self.W, self.A, self.unique_rows, self.coal, self.num_unique,
@@ -249,14 +268,15 @@ class EmbeddingTrainer:
                         self.seg_offsets, self.casted_src, self.num_unique, self.workspace,
                         stream)
         tc_embed_coalesce(self.expanded, num_pairs, self.seg_offsets, self.casted_src,
-                          self.num_unique, self.max_unique, self.coal, stream)
+                          self.num_unique, self.max_unique, self.coal, self.bwd_workspace,
+                          stream)
 
     def backward_update(self, grad_out, stream=None, store_coal=False):
         """backward + update in one pass (coal stored only if store_coal)."""
         tc_embed_backward_update(grad_out, self.seg_offsets, self.casted_src, self.unique_rows,
                                  self.num_unique, self.max_unique, self.W, self.A, self.opt_kind,
                                  self.lr, self.eps, self.gamma,
-                                 self.coal if store_coal else None, stream)
+                                 self.coal if store_coal else None, self.bwd_workspace, stream)
 
     def step(self, table_row_offset, indices, bag_offsets, num_pairs, grad_out, stream=None,
              fused=True):

@@ -37,12 +37,24 @@ def test_every_declared_symbol_is_exported(header):
 
 
 def test_version_and_status_strings(tc):
-    assert tc.tc_abi_version() == 3
+    assert tc.tc_abi_version() == 4
     lib = tc._lib
     for code, name in enumerate(["TC_OK", "TC_ERR_INVALID_ARG", "TC_ERR_UNSUPPORTED",
                                  "TC_ERR_WORKSPACE", "TC_ERR_HIP"]):
         assert lib.tc_status_string(code).decode() == name
     assert lib.tc_status_string(99).decode() == "TC_ERR_UNKNOWN"
+
+
+def test_backward_workspace_bytes(tc):
+    f = tc.tc_backward_workspace_bytes
+    assert f(127, 64) == 0 and f(0, 64) == 0 and f(-5, 64) == 0 and f(128, 64) > 0
+    assert f(10 ** 6, 0) == 0 and f(10 ** 6, 1028) == 0 and f(2 ** 31, 64) == 0
+    sizes = [f(n, 64) for n in (128, 2048, 4096, 10 ** 5, 10 ** 6, 10 ** 7)]
+    assert sizes == sorted(sizes) and all(s % 256 == 0 for s in sizes)
+    # piece sums (a row of dim floats per 1024 pairs) plus the work lists
+    n = 10 ** 7
+    assert n // 1024 * 64 * 4 <= f(n, 64) <= n * (64 / 256 + 0.15)
+    assert f(10 ** 6, 256) > f(10 ** 6, 64)
 
 
 def test_workspace_bytes(tc):
@@ -141,8 +153,11 @@ def test_backward_and_update_reject_bad_arguments(tc):
     def bwd(**k):
         return lib.tc_embed_backward(k.get("g", h.fp()), k.get("nb", 10), k.get("dim", 8),
                                      k.get("so", h.ip()), k.get("cs", h.ip()), k.get("nu", h.ip()),
-                                     k.get("mu", 10), k.get("coal", h.fp()), None)
+                                     k.get("mu", 10), k.get("coal", h.fp()), k.get("ws", None),
+                                     k.get("wsb", 0), None)
     assert bwd(dim=10) == tc.TC_ERR_UNSUPPORTED
+    assert bwd(wsb=4096) == tc.TC_ERR_INVALID_ARG and "workspace" in _err(tc)
+    assert bwd(ws=h.fp(misalign=True), wsb=4096) == tc.TC_ERR_INVALID_ARG
     assert bwd(mu=-1) == tc.TC_ERR_INVALID_ARG
     assert bwd(nu=None) == tc.TC_ERR_INVALID_ARG
     assert bwd(coal=h.fp(misalign=True)) == tc.TC_ERR_UNSUPPORTED
@@ -175,7 +190,7 @@ def test_backward_and_update_reject_bad_arguments(tc):
             k.get("g", h.fp()), k.get("nb", 10), k.get("dim", 8), k.get("so", h.ip()),
             k.get("cs", h.ip()), k.get("ur", h.ip()), k.get("nu", h.ip()), k.get("mu", 10),
             k.get("W", h.fp()), k.get("A", None), k.get("rows", 100), k.get("opt", 0), 0.01, 1e-8,
-            k.get("gamma", 0.9), k.get("coal", None), None)
+            k.get("gamma", 0.9), k.get("coal", None), k.get("ws", None), k.get("wsb", 0), None)
     assert fused(dim=6) == tc.TC_ERR_UNSUPPORTED
     assert fused(mu=-1) == tc.TC_ERR_INVALID_ARG
     assert fused(rows=2 ** 31) == tc.TC_ERR_INVALID_ARG
@@ -186,6 +201,7 @@ def test_backward_and_update_reject_bad_arguments(tc):
     assert fused(opt=3, A=h.fp()) == tc.TC_ERR_UNSUPPORTED      # row-wise: two calls
     assert "row-wise" in _err(tc)
     assert fused(opt=5, A=h.fp()) == tc.TC_ERR_INVALID_ARG
+    assert fused(wsb=1024) == tc.TC_ERR_INVALID_ARG
     assert fused(W=None) == tc.TC_ERR_INVALID_ARG and "null" in _err(tc)
     assert fused(ur=None) == tc.TC_ERR_INVALID_ARG
     assert fused(coal=h.fp(misalign=True)) == tc.TC_ERR_UNSUPPORTED
@@ -204,8 +220,10 @@ def test_backward_and_update_reject_bad_arguments(tc):
     def coalesce(**k):
         return lib.tc_embed_coalesce(k.get("e", h.fp()), k.get("n", 10), k.get("dim", 8),
                                      k.get("so", h.ip()), k.get("sp", h.ip()), k.get("nu", h.ip()),
-                                     k.get("mu", 10), k.get("coal", h.fp()), None)
+                                     k.get("mu", 10), k.get("coal", h.fp()), k.get("ws", None),
+                                     k.get("wsb", 0), None)
     assert coalesce(dim=1030) == tc.TC_ERR_UNSUPPORTED
+    assert coalesce(wsb=64) == tc.TC_ERR_INVALID_ARG
     assert coalesce(mu=-3) == tc.TC_ERR_INVALID_ARG
     assert coalesce(sp=None) == tc.TC_ERR_INVALID_ARG
     assert coalesce(mu=0) == tc.TC_OK

@@ -1,17 +1,22 @@
 """All five workloads at full size, one step each, in the launch
-configuration the benchmark times (backward and update fused; the coalesced
-rows are also stored, to be checked). The casted index is compared with the
-oracle's in full (bit for bit); forward rows, coalesced gradients and
-updated rows are compared on samples the oracle computes on their own: a
-sampled bag needs only its own pairs, a sampled table row only the pairs
-that gather it (kept in input order, so the sum order is unchanged)."""
+configuration the benchmark times (backward and update fused, with the
+backward workspace, so segments of 2048 pairs or more are summed in pieces;
+the coalesced rows are also stored, to be checked). The casted index is
+compared with the oracle's in full (bit for bit); forward rows, coalesced
+gradients and updated rows are compared on samples the oracle computes on
+their own: a sampled bag needs only its own pairs, a sampled table row only
+the pairs that gather it (kept in input order, so the sum order is
+unchanged). A split row's expected sum is composed from the oracle's sums
+in the documented piece order, and it is also checked against the fp64
+oracle's sequential sum within the tolerance."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
 from paper_2010_13100_amd import workload as wl
-from tests.gpu_harness import GpuRun, assert_close, compare_cast
+from tests.gpu_harness import (SPLIT_PAIRS, GpuRun, assert_close, compare_cast, piecewise_row,
+                               scatter)
 
 pytestmark = pytest.mark.gpu
 
@@ -21,7 +26,8 @@ def test_full_size_step(cfg):
     w = wl.WORKLOADS[cfg]
     b = wl.make_batch(w, step=0)
     print(f"\n[{cfg}] {w.name}: {b.num_pairs} pairs", flush=True)
-    run = GpuRun(w, max_pairs=b.num_pairs)
+    run = GpuRun(w, max_pairs=b.num_pairs, split_long=True)
+    assert run.split_cap >= b.num_pairs
     run.run_step(b, with_casted_dst=True, fused=True, store_coal=True)
     t = run.trainer
     orc = oracle.Oracle("f32")
@@ -54,17 +60,23 @@ def test_full_size_step(cfg):
     mask = np.isin(src, rows)
     ref_coal, ref_rows = orc.coalesce(src[mask], orc.expand(dst[mask], b.grad_out))
     assert np.array_equal(ref_rows, rows)
+    orc64 = oracle.Oracle("f64")
+    seq64, _ = orc64.coalesce(src[mask], orc64.expand(dst[mask], b.grad_out))
+    split = np.flatnonzero(seg[pick] >= SPLIT_PAIRS)
+    for k in split:   # the row's bags in input order = its segment in sorted order
+        ref_coal[k] = piecewise_row(orc, dst[src == rows[k]], b.grad_out)
     got_coal = t.coal.index_select(0, torch.from_numpy(pick).cuda()).cpu().numpy()
     assert_close(got_coal, ref_coal, f"{cfg} coalesced gradient (sampled rows)", bitwise=True)
+    if len(split):
+        assert_close(got_coal[split], seq64[split], f"{cfg} split rows vs fp64 sums")
     tbl = wl.table_rows(w, rows)
-    if w.optimizer == "sgd":
-        orc.scatter_sgd(rows, ref_coal, np.float32(w.lr), tbl, rows)
-    else:
-        acc = np.zeros_like(tbl)
-        orc.scatter_adagrad(rows, ref_coal, np.float32(w.lr), np.float32(w.eps), tbl, acc, rows)
+    acc = None if w.optimizer == "sgd" else np.zeros_like(tbl)
+    scatter(orc, w, rows, ref_coal, tbl, acc, rows)
+    if acc is not None:
         assert_close(run.acc_rows(rows), acc, f"{cfg} accumulator (sampled rows)", bitwise=True)
     assert_close(run.rows(rows), tbl, f"{cfg} updated rows (sampled)", bitwise=True)
-    print(f"[{cfg}] longest segment {seg.max()}, sampled rows {len(rows)} match", flush=True)
+    print(f"[{cfg}] longest segment {seg.max()}, sampled rows {len(rows)} match "
+          f"({len(split)} split)", flush=True)
 
     # rows the step does not touch keep their initial values
     cand = rng.integers(0, w.total_rows, size=5000)
