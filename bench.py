@@ -51,11 +51,12 @@ KERNEL_SOURCES = {
 }
 KERNEL_NAMES = {
     "forward": ["k_forward"],
-    "backward": ["k_backward_long", "k_backward_short"],
-    "backward_update": ["k_backward_long", "k_backward_short"],
+    # with the backward workspace, as the step runs them
+    "backward": ["k_backward_init", "k_backward_short", "k_backward_list"],
+    "backward_update": ["k_backward_init", "k_backward_short", "k_backward_list"],
     "update": ["k_sparse_update"],
-    "cast": ["k_build_keys", "k_radix_hist", "k_radix_scan", "k_radix_scatter", "k_seg_count",
-             "k_seg_scan", "k_seg_write"],
+    "cast": ["k_cast_small", "k_build_keys", "k_radix_hist", "k_radix_scan", "k_radix_scatter",
+             "k_seg_count", "k_seg_scan", "k_seg_write"],
 }
 
 
@@ -79,7 +80,7 @@ def load_traffic(call: str, workload: str):
 
 
 def run_ab(args, w, trainer, dbat, stream):
-    """The paper's backward A/B (Sec. VI-B) on this GPU: baseline gradient
+    """The paper's backward A/B (Sec. VI-A) on this GPU: baseline gradient
     expand-coalesce (expand, stable argsort, Algorithm 1 accumulate) against
     Tensor Casting (cast, Algorithm 3 gather-reduce), same batches, both
     producing the coalesced gradient rows. Each variant's calls of one step
@@ -363,7 +364,7 @@ def measure_step(args, w, cfg_name, trainer, dbat, stream, unfused, traffic_key)
 
 
 def run_sweep(args, base, cfg_name, dev):
-    """The sensitivity study (Sec. VI-E): for each batch size or embedding
+    """The sensitivity study (Sec. VI-D): for each batch size or embedding
     dimension, the step (steps/s, dominant call's HBM fraction) and the
     backward A/B (baseline expand-coalesce against Tensor Casting). One JSON
     line per point."""
