@@ -141,14 +141,14 @@ __device__ __forceinline__ void sink_value(const RowSink &k, int64_t u, int32_t 
     }
 }
 
-// A lane group's float4 chunks of coalesced row u.
+// A lane group's float4 chunks of coalesced row u, whose table row is r
+// (rows[u], loaded by the caller together with the segment's offsets).
 template <int LANES, int CHUNKS>
-__device__ __forceinline__ void sink_group(const RowSink &k, int64_t u, int32_t dim, int sub,
-                                           const float4 (&acc)[CHUNKS]) {
+__device__ __forceinline__ void sink_group(const RowSink &k, int64_t u, int64_t r, int32_t dim,
+                                           int sub, const float4 (&acc)[CHUNKS]) {
     if (k.coal) group_store<LANES, CHUNKS>(k.coal + u * dim, dim, sub, acc);
     if (k.W) {
         const int d4 = dim >> 2;
-        const int64_t r = k.rows[u];
         float *wrow = k.W + r * dim;
 #pragma unroll
         for (int c = 0; c < CHUNKS; ++c) {
@@ -550,9 +550,11 @@ __global__ __launch_bounds__(kBlock) void k_backward_short(
         bool mine = false;
         bool listed = false;  // a covered long segment, not split
         int32_t len = 0;
+        int64_t r = 0;  // the table row the sink updates
         if (o < num) {
             beg = offsets[o];
             end = offsets[o + 1];
+            if (sink.W) r = sink.rows[o];
             len = end - beg;
             const bool covered = len >= kLongSegment && int64_t(beg) + len <= ws.cap_pairs;
             // without a workspace long segments go to k_backward_long; with
@@ -589,7 +591,7 @@ __global__ __launch_bounds__(kBlock) void k_backward_short(
 #pragma unroll
         for (int c = 0; c < CHUNKS; ++c) acc[c] = make_float4(0.f, 0.f, 0.f, 0.f);
         group_range_sum<LANES, CHUNKS>(grad, dim, ids, 0, beg, end, sub, acc);
-        if (mine) sink_group<LANES, CHUNKS>(sink, o, dim, sub, acc);
+        if (mine) sink_group<LANES, CHUNKS>(sink, o, r, dim, sub, acc);
     }
 }
 
