@@ -120,24 +120,42 @@ struct RowSink {
     float lr, eps, gamma, omg;  // omg = 1 - gamma
 };
 
-// One lane's column `col` of coalesced row u.
+// The table (and accumulator) value one lane's sink_value updates: column
+// `col` of table row rows[u]. A consumer loads it before running the
+// segment's chain, so that its two dependent loads overlap the chain.
+struct SinkVal {
+    int64_t at;
+    float w, a;
+};
+
+__device__ __forceinline__ SinkVal sink_value_load(const RowSink &k, int64_t u, int32_t dim,
+                                                   int32_t col) {
+    SinkVal v{0, 0.f, 0.f};
+    if (k.W && col < dim) {
+        v.at = int64_t(k.rows[u]) * dim + col;
+        v.w = k.W[v.at];
+        if (k.kind != TC_OPT_SGD) v.a = k.A[v.at];
+    }
+    return v;
+}
+
+// One lane's column `col` of coalesced row u, with its table value in v.
 __device__ __forceinline__ void sink_value(const RowSink &k, int64_t u, int32_t dim, int32_t col,
-                                           float g) {
+                                           float g, const SinkVal &v) {
     if (k.coal) k.coal[u * dim + col] = g;
     if (k.W) {
-        const int64_t at = int64_t(k.rows[u]) * dim + col;
-        float w = k.W[at];
+        float w = v.w;
         if (k.kind == TC_OPT_SGD) {
             w = sgd_step(w, g, k.lr);
         } else {
-            float a = k.A[at];
+            float a = v.a;
             if (k.kind == TC_OPT_ADAGRAD)
                 adagrad_step(w, a, g, k.lr, k.eps);
             else
                 rmsprop_step(w, a, g, k.lr, k.eps, k.gamma, k.omg);
-            k.A[at] = a;
+            k.A[v.at] = a;
         }
-        k.W[at] = w;
+        k.W[v.at] = w;
     }
 }
 
@@ -421,7 +439,7 @@ __device__ void finish_piece(const SplitWs &ws, const RowSink &sink, int32_t dim
     float tot = 0.f;
     for (int32_t k = 0; k < n; ++k)
         tot = tot + ws.partial[int64_t(piece_begin(beg, len, n, k) / kPieceMin) * dim + col];
-    sink_value(sink, u, dim, col, tot);
+    sink_value(sink, u, dim, col, tot, sink_value_load(sink, u, dim, col));
 }
 
 // Long segments without a workspace. Each block (range x, part y) scans a
@@ -469,8 +487,10 @@ __global__ __launch_bounds__(kLongThreads) void k_backward_long(
                 const int32_t beg = __builtin_amdgcn_readlane(o0, j);
                 const int32_t len = __builtin_amdgcn_readlane(o1, j) - beg;
                 const int64_t seg = c0 + int64_t(kWave) * i + j;
+                SinkVal sv{0, 0.f, 0.f};
+                if (w == 0) sv = sink_value_load(sink, seg, dim, col);
                 const float acc = run_chain(lds, grad, dim, ids, beg, len, w, part, col);
-                if (w == 0 && col < dim) sink_value(sink, seg, dim, col, acc);
+                if (w == 0 && col < dim) sink_value(sink, seg, dim, col, acc, sv);
             }
         }
     }
@@ -515,8 +535,10 @@ __global__ __launch_bounds__(kLongThreads, 3) void k_backward_list(
             const float acc = run_chain(lds, grad, dim, ids, p0, p1 - p0, w, part, col);
             if (w == 0) finish_piece(ws, sink, dim, part, col, u, beg, len, n, q, acc);
         } else {
+            SinkVal sv{0, 0.f, 0.f};
+            if (w == 0) sv = sink_value_load(sink, u, dim, col);
             const float acc = run_chain(lds, grad, dim, ids, beg, len, w, part, col);
-            if (w == 0 && col < dim) sink_value(sink, u, dim, col, acc);
+            if (w == 0 && col < dim) sink_value(sink, u, dim, col, acc, sv);
         }
         lds_barrier();  // every wavefront is past this item
         if (threadIdx.x == 0) next_item = ahead;
