@@ -56,7 +56,7 @@ KERNEL_NAMES = {
     "backward_update": ["k_backward_init", "k_backward_short", "k_backward_list"],
     "update": ["k_sparse_update"],
     "cast": ["k_cast_small", "k_build_keys", "k_radix_hist", "k_radix_scan", "k_radix_scatter",
-             "k_seg_count", "k_seg_scan", "k_seg_write"],
+             "k_seg_count", "k_seg_write"],
 }
 
 

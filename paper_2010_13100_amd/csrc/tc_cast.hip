@@ -16,8 +16,8 @@
 //     histogram. The last pass writes the values straight into casted_src.
 //  3. Segment build (the scan and cumulative sum of Algorithm 2):
 //       k_seg_count  heads (key differs from its predecessor) per tile
-//       k_seg_scan   exclusive scan of tile head counts -> *num_unique
-//       k_seg_write  casted_dst, unique_rows, seg_offsets
+//       k_seg_write  casted_dst, unique_rows, seg_offsets, *num_unique (each
+//                    block sums the head counts of the tiles before it)
 //
 // Sort segments. The pairs of table t are contiguous in the input
 // (bag-major CSR, tables in order) and so are their rows in the output. When
@@ -430,41 +430,25 @@ __global__ __launch_bounds__(kBlock) void k_seg_count(const int32_t *__restrict_
     }
 }
 
-// 3b. exclusive scan of the tile head counts (one block); total -> *num_unique.
-__global__ __launch_bounds__(kBlock) void k_seg_scan(int32_t *__restrict__ tile_heads,
-                                                     int32_t num_tiles,
-                                                     int32_t *__restrict__ num_unique) {
-    constexpr int kPer = 4;
-    int32_t carry = 0;
-    for (int32_t base = 0; base < num_tiles; base += kBlock * kPer) {
-        int32_t v[kPer], s = 0;
-#pragma unroll
-        for (int k = 0; k < kPer; ++k) {
-            const int32_t i = base + threadIdx.x * kPer + k;
-            v[k] = i < num_tiles ? tile_heads[i] : 0;
-            s += v[k];
-        }
-        int32_t tot;
-        int32_t p = block_exclusive_scan(s, &tot) + carry;
-#pragma unroll
-        for (int k = 0; k < kPer; ++k) {
-            const int32_t i = base + threadIdx.x * kPer + k;
-            if (i < num_tiles) tile_heads[i] = p;
-            p += v[k];
-        }
-        carry += tot;
-    }
-    if (threadIdx.x == 0) *num_unique = carry;
-}
-
-// 3c. casted_dst (inclusive head count - 1), unique_rows and seg_offsets.
+// 3b. casted_dst (inclusive head count - 1), unique_rows and seg_offsets.
+// Each block adds up the head counts of the tiles before it (a few loads per
+// thread even for thousands of tiles, so no separate scan kernel); the last
+// block writes *num_unique.
 __global__ __launch_bounds__(kBlock) void k_seg_write(
     const int32_t *__restrict__ keys, int64_t n, const int32_t *__restrict__ tile_heads,
     int32_t *__restrict__ unique_rows, int32_t *__restrict__ seg_offsets,
-    int32_t *__restrict__ casted_dst) {
+    int32_t *__restrict__ casted_dst, int32_t *__restrict__ num_unique) {
     __shared__ int32_t wsum[kSortWaves];
+    __shared__ int32_t before;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
     const int64_t base = int64_t(blockIdx.x) * kTile + int64_t(w) * kWaveSpan;
+    {
+        int32_t part = 0;
+        for (int32_t t = tid; t < int32_t(blockIdx.x); t += kBlock) part += tile_heads[t];
+        int32_t tot;
+        block_exclusive_scan(part, &tot);
+        if (tid == 0) before = tot;
+    }
     int32_t key[kItems];
     uint64_t heads[kItems];
     int32_t c = 0;
@@ -478,8 +462,13 @@ __global__ __launch_bounds__(kBlock) void k_seg_write(
     }
     if (lane == 0) wsum[w] = c;
     __syncthreads();
-    int32_t run = tile_heads[blockIdx.x];
+    int32_t run = before;
     for (int ww = 0; ww < w; ++ww) run += wsum[ww];
+    if (blockIdx.x == gridDim.x - 1 && tid == 0) {
+        int32_t total = before;
+        for (int ww = 0; ww < kSortWaves; ++ww) total += wsum[ww];
+        *num_unique = total;
+    }
     const uint64_t le = lanemask_lt(lane) | (uint64_t(1) << lane);
 #pragma unroll
     for (int i = 0; i < kItems; ++i) {
@@ -854,11 +843,8 @@ tc_status cast_impl(const char *what, bool positions, const int64_t *table_row_o
     k_seg_count<<<seg_tiles, kBlock, 0, stream>>>(sorted_keys, num_pairs, heads);
     tc_status st = check_launch("k_seg_count");
     if (st != TC_OK) return st;
-    k_seg_scan<<<1, kBlock, 0, stream>>>(heads, seg_tiles, num_unique);
-    st = check_launch("k_seg_scan");
-    if (st != TC_OK) return st;
     k_seg_write<<<seg_tiles, kBlock, 0, stream>>>(sorted_keys, num_pairs, heads, unique_rows,
-                                                  seg_offsets, casted_dst);
+                                                  seg_offsets, casted_dst, num_unique);
     return check_launch("k_seg_write");
 }
 }  // namespace
