@@ -71,6 +71,10 @@ constexpr int32_t kSplitPairs = TC_BACKWARD_SPLIT_PAIRS;
 constexpr int32_t kPieceMin = 1024;
 constexpr int32_t kMaxPieces = 32;
 static_assert(kSplitPairs >= 2 * kPieceMin && kPieceMin >= kLongSegment, "piece sizes");
+// Long segments of at least kBigLong pairs are handed out before the shorter
+// ones, so that the work left at the end is small (the workgroups finish
+// together).
+constexpr int32_t kBigLong = 512;
 
 // The backward workspace. The lists are filled by k_backward_short and
 // drained by k_backward_list; k_backward_init zeroes the counters first.
@@ -79,7 +83,10 @@ static_assert(kSplitPairs >= 2 * kPieceMin && kPieceMin >= kLongSegment, "piece 
 // of at least kSplitPairs pairs, and pieces of at least kPieceMin pairs, so
 // beg / kSplitPairs and (first pair of the piece) / kPieceMin name them
 // without collisions.
-//   ctr[0], ctr[1]   entries in pieces[] and longs[]; ctr[2] next work item
+//   ctr[0]           entries in pieces[]
+//   ctr[1], ctr[2]   long segments of at least / under kBigLong pairs, kept
+//                    from the front / from the back of longs[]
+//   ctr[3]           next work item
 //   pieces[k]        {u, beg, len, q}: piece q of split segment u
 //   longs[k]         {u, beg, len, 0}: a covered long segment, not split
 //   seg_done[(beg / kSplitPairs) * parts + p]  pieces of part p finished
@@ -286,6 +293,7 @@ __device__ void long_producer(LongLds &lds, __amdgpu_buffer_rsrc_t id_rsrc, int3
 #pragma unroll
     for (int e = 0; e < kIdAhead; ++e) iv[e] = load_ids(e);
     static_assert(kAhead == 3, "the prologue issues kAhead chunks");
+    static_assert(kIdAhead > 4, "the prologue uses the ids of chunks 0..4");
     issue(Int<0>{}, Int<0>{}, 0);
     issue(Int<1>{}, Int<1>{}, 1);
     issue(Int<2>{}, Int<2>{}, 2);
@@ -497,7 +505,8 @@ __global__ __launch_bounds__(kLongThreads) void k_backward_long(
 }
 
 // Long segments with a workspace: persistent blocks take work items
-// (index / parts = list entry, pieces first; index % parts = part) from an
+// (index / parts = list entry: pieces, then long segments of at least
+// kBigLong pairs, then the shorter ones; index % parts = part) from an
 // agent-scope counter until the lists are drained. The next item is fetched
 // while the current one runs.
 __global__ __launch_bounds__(kLongThreads, 3) void k_backward_list(
@@ -508,10 +517,11 @@ __global__ __launch_bounds__(kLongThreads, 3) void k_backward_list(
     const int lane = threadIdx.x & (kWave - 1);
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int32_t np = min(ws.ctr[0], ws.max_pieces);
-    const int32_t nl = min(ws.ctr[1], ws.max_longs);
-    const int64_t total = int64_t(np + nl) * ws.parts;
+    const int32_t nb = min(ws.ctr[1], ws.max_longs);
+    const int32_t ns = min(ws.ctr[2], ws.max_longs - nb);
+    const int64_t total = int64_t(np + nb + ns) * ws.parts;
     if (threadIdx.x == 0)
-        next_item = __hip_atomic_fetch_add(&ws.ctr[2], 1, __ATOMIC_RELAXED,
+        next_item = __hip_atomic_fetch_add(&ws.ctr[3], 1, __ATOMIC_RELAXED,
                                            __HIP_MEMORY_SCOPE_AGENT);
     lds_barrier();
     int32_t item = next_item;
@@ -519,11 +529,13 @@ __global__ __launch_bounds__(kLongThreads, 3) void k_backward_list(
     while (item < total) {
         int32_t ahead = 0;
         if (threadIdx.x == 0)
-            ahead = __hip_atomic_fetch_add(&ws.ctr[2], 1, __ATOMIC_RELAXED,
+            ahead = __hip_atomic_fetch_add(&ws.ctr[3], 1, __ATOMIC_RELAXED,
                                            __HIP_MEMORY_SCOPE_AGENT);
         const int32_t k = item / ws.parts, part = item % ws.parts;
         const int32_t col = part * kPartCols + lane;
-        const int4 e = k < np ? ws.pieces[k] : ws.longs[k - np];
+        const int4 e = k < np        ? ws.pieces[k]
+                       : k < np + nb ? ws.longs[k - np]
+                                     : ws.longs[ws.max_longs - 1 - (k - np - nb)];
         const int32_t u = __builtin_amdgcn_readfirstlane(e.x);
         const int32_t beg = __builtin_amdgcn_readfirstlane(e.y);
         const int32_t len = __builtin_amdgcn_readfirstlane(e.z);
@@ -548,7 +560,7 @@ __global__ __launch_bounds__(kLongThreads, 3) void k_backward_list(
 }
 
 __global__ void k_backward_init(SplitWs ws) {
-    if (threadIdx.x < 3) ws.ctr[threadIdx.x] = 0;
+    if (threadIdx.x < 4) ws.ctr[threadIdx.x] = 0;
 }
 
 // Short segments: one lane group per segment, as the forward; long ones are
@@ -597,17 +609,22 @@ __global__ __launch_bounds__(kBlock) void k_backward_short(
             }
             if (!mine) end = beg;
         }
-        // one counter update per wavefront for the long-segment list
-        const uint64_t lm = __ballot(listed);
-        if (lm) {
+        // one counter update per wavefront and list: big ones from the
+        // front of longs[], the others from the back
+#pragma unroll
+        for (int big = 1; big >= 0; --big) {
+            const bool mine_list = listed && (len >= kBigLong) == bool(big);
+            const uint64_t lm = __ballot(mine_list);
+            if (lm == 0) continue;
             const int leader = __builtin_ctzll(lm);
             int32_t at = 0;
             if (lane == leader)
-                at = __hip_atomic_fetch_add(&ws.ctr[1], __builtin_popcountll(lm), __ATOMIC_RELAXED,
-                                            __HIP_MEMORY_SCOPE_AGENT);
+                at = __hip_atomic_fetch_add(&ws.ctr[big ? 1 : 2], __builtin_popcountll(lm),
+                                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             at = __builtin_amdgcn_readlane(at, leader) +
                  __builtin_popcountll(lm & ((uint64_t(1) << lane) - 1));
-            if (listed && at < ws.max_longs) ws.longs[at] = make_int4(int32_t(o), beg, len, 0);
+            if (mine_list && at < ws.max_longs)
+                ws.longs[big ? at : ws.max_longs - 1 - at] = make_int4(int32_t(o), beg, len, 0);
         }
         float4 acc[CHUNKS];
 #pragma unroll
