@@ -21,13 +21,16 @@ from tests.gpu_harness import (SPLIT_PAIRS, GpuRun, assert_close, compare_cast, 
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("cfg", ["c1", "c2", "c3", "c4", "c5"])
-def test_full_size_step(cfg):
+@pytest.mark.parametrize("cfg,split", [("c1", True), ("c2", True), ("c3", True), ("c4", True),
+                                       ("c5", True), ("c2", False), ("c3", False)])
+def test_full_size_step(cfg, split):
+    """split: with the backward workspace (as the benchmark runs), or without
+    it (every segment one ordered chain, the hottest rows included)."""
     w = wl.WORKLOADS[cfg]
     b = wl.make_batch(w, step=0)
-    print(f"\n[{cfg}] {w.name}: {b.num_pairs} pairs", flush=True)
-    run = GpuRun(w, max_pairs=b.num_pairs, split_long=True)
-    assert run.split_cap >= b.num_pairs
+    print(f"\n[{cfg} split={split}] {w.name}: {b.num_pairs} pairs", flush=True)
+    run = GpuRun(w, max_pairs=b.num_pairs, split_long=split)
+    assert run.split_cap >= b.num_pairs if split else run.split_cap == 0
     run.run_step(b, with_casted_dst=True, fused=True, store_coal=True)
     t = run.trainer
     orc = oracle.Oracle("f32")
@@ -62,13 +65,13 @@ def test_full_size_step(cfg):
     assert np.array_equal(ref_rows, rows)
     orc64 = oracle.Oracle("f64")
     seq64, _ = orc64.coalesce(src[mask], orc64.expand(dst[mask], b.grad_out))
-    split = np.flatnonzero(seg[pick] >= SPLIT_PAIRS)
-    for k in split:   # the row's bags in input order = its segment in sorted order
+    pieces = np.flatnonzero(seg[pick] >= SPLIT_PAIRS) if run.split_cap else np.zeros(0, int)
+    for k in pieces:   # the row's bags in input order = its segment in sorted order
         ref_coal[k] = piecewise_row(orc, dst[src == rows[k]], b.grad_out)
     got_coal = t.coal.index_select(0, torch.from_numpy(pick).cuda()).cpu().numpy()
     assert_close(got_coal, ref_coal, f"{cfg} coalesced gradient (sampled rows)", bitwise=True)
-    if len(split):
-        assert_close(got_coal[split], seq64[split], f"{cfg} split rows vs fp64 sums")
+    if len(pieces):
+        assert_close(got_coal[pieces], seq64[pieces], f"{cfg} split rows vs fp64 sums")
     tbl = wl.table_rows(w, rows)
     acc = None if w.optimizer == "sgd" else np.zeros_like(tbl)
     scatter(orc, w, rows, ref_coal, tbl, acc, rows)
@@ -76,7 +79,7 @@ def test_full_size_step(cfg):
         assert_close(run.acc_rows(rows), acc, f"{cfg} accumulator (sampled rows)", bitwise=True)
     assert_close(run.rows(rows), tbl, f"{cfg} updated rows (sampled)", bitwise=True)
     print(f"[{cfg}] longest segment {seg.max()}, sampled rows {len(rows)} match "
-          f"({len(split)} split)", flush=True)
+          f"({len(pieces)} split)", flush=True)
 
     # rows the step does not touch keep their initial values
     cand = rng.integers(0, w.total_rows, size=5000)
