@@ -21,6 +21,8 @@
  *   tc_argsort_rows    stable argsort of the pairs by row (Algorithm 1's ArgSort)
  *   tc_embed_coalesce  Algorithm 1's ordered accumulate of the expanded rows
  *
+ * tc_check_index checks an index array on the device before it is trusted.
+ *
  * Conventions shared by every call
  * --------------------------------
  * Pointers are DEVICE pointers owned by the caller unless a comment says
@@ -50,8 +52,10 @@
  *  - `dim` must be a multiple of 4 in [4, 1024], and every float pointer must
  *    be 16-byte aligned (TC_ERR_UNSUPPORTED otherwise); num_pairs and
  *    total_rows must be below 2^31.
- *  - Out-of-range indices or malformed offsets are not detected and give
- *    undefined results.
+ *  - Out-of-range indices or malformed offsets are not detected by the
+ *    training calls and give undefined results (reads and writes outside
+ *    the table included); tc_check_index checks an index array on the
+ *    device without copying anything to the host.
  *
  * Arithmetic: fp32 values, fp32 accumulation. Sums are taken one term after
  * another, from +0, in the order of the index array (forward) or of the
@@ -75,7 +79,7 @@
 extern "C" {
 #endif
 
-#define TC_ABI_VERSION 4
+#define TC_ABI_VERSION 5
 
 /* Segments at least this long are summed in pieces when a backward
  * workspace covers them (tc_embed_backward). */
@@ -281,6 +285,40 @@ tc_status tc_embed_backward_update(const float *grad_out, int32_t num_bags, int3
                                    int64_t total_rows, int32_t opt_kind, float lr, float eps,
                                    float gamma, float *coal_grad, void *workspace,
                                    size_t workspace_bytes, hipStream_t stream);
+
+/* What tc_check_index found (report[0]). */
+typedef enum tc_index_problem {
+    TC_INDEX_OK = 0,
+    TC_INDEX_BAD_TABLE_OFFSETS = 1,  /* table_row_offset[0] != 0, a decrease, or [T] != total_rows */
+    TC_INDEX_BAD_BAG_OFFSETS = 2,    /* bag_offsets[0] != 0, a decrease, or [T*B] != num_pairs */
+    TC_INDEX_OUT_OF_RANGE = 3        /* an index < 0, >= its table's rows, or >= max_table_rows */
+} tc_index_problem;
+
+/*
+ * Checks the index array of a step (the (src, dst) pairs of Sec. II-B in the
+ * layout above) on the device, for callers whose indices are not trusted:
+ *   table_row_offset [T+1]: starts at 0, never decreases, ends at total_rows
+ *   bag_offsets      [T*B+1]: starts at 0, never decreases, ends at num_pairs
+ *   indices          [num_pairs]: pair j of table t (the table whose bags
+ *                    hold position j) satisfies 0 <= indices[j] <
+ *                    table_row_offset[t+1] - table_row_offset[t], and
+ *                    indices[j] < max_table_rows when max_table_rows > 0
+ *                    (the bound tc_cast_index takes)
+ *   report           device int64[2], written: report[0] is a
+ *                    tc_index_problem, report[1] the lowest entry t
+ *                    (table_row_offset), bag g (bag_offsets) or pair j
+ *                    (indices) where it holds, or -1 if there is none. Of
+ *                    several problems the lowest kind is reported, then the
+ *                    lowest position; the result does not depend on the
+ *                    launch configuration. 8-byte aligned.
+ * Arguments are those of tc_cast_index; the library does not read report
+ * back: the caller copies it after the stream reaches it. Never reads
+ * outside the arrays' stated sizes, whatever their contents.
+ */
+tc_status tc_check_index(const int64_t *table_row_offset, int32_t num_tables,
+                         int32_t bags_per_table, int64_t total_rows, int64_t max_table_rows,
+                         const int32_t *indices, const int32_t *bag_offsets, int64_t num_pairs,
+                         int64_t *report, hipStream_t stream);
 
 /* Static text for a status code. */
 const char *tc_status_string(tc_status status);

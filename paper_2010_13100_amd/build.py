@@ -26,7 +26,7 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", "-shared", "-ffp-contract=off",
 
 LIBS = {
     "libtc.so": ["tc_api.hip", "tc_gather_reduce.hip", "tc_backward.hip", "tc_cast.hip",
-                 "tc_update.hip"],
+                 "tc_update.hip", "tc_check.hip"],
     "libtc_workload.so": ["workload_fill.hip"],
 }
 

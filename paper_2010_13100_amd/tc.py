@@ -15,6 +15,7 @@ import torch
 from . import build as _build
 
 TC_OK, TC_ERR_INVALID_ARG, TC_ERR_UNSUPPORTED, TC_ERR_WORKSPACE, TC_ERR_HIP = range(5)
+TC_INDEX_OK, TC_INDEX_BAD_TABLE_OFFSETS, TC_INDEX_BAD_BAG_OFFSETS, TC_INDEX_OUT_OF_RANGE = range(4)
 TC_OPT_SGD, TC_OPT_ADAGRAD, TC_OPT_RMSPROP, TC_OPT_ROWWISE_ADAGRAD = range(4)
 OPTIMIZERS = {"sgd": TC_OPT_SGD, "adagrad": TC_OPT_ADAGRAD, "rmsprop": TC_OPT_RMSPROP,
               "rowwise_adagrad": TC_OPT_ROWWISE_ADAGRAD}
@@ -37,6 +38,7 @@ _SIGNATURES = {
                                _vp, _sz, _vp]),
     "tc_embed_expand": (_i32, [_vp, _i32, _i32, _vp, _i64, _vp, _vp]),
     "tc_embed_coalesce": (_i32, [_vp, _i64, _i32, _vp, _vp, _vp, _i64, _vp, _vp, _sz, _vp]),
+    "tc_check_index": (_i32, [_vp, _i32, _i32, _i64, _i64, _vp, _vp, _i64, _vp, _vp]),
     "tc_status_string": (ctypes.c_char_p, [_i32]),
     "tc_last_error": (ctypes.c_char_p, []),
     "tc_abi_version": (_i32, []),
@@ -117,6 +119,15 @@ def tc_cast_index(table_row_offset, num_tables, bags_per_table, total_rows, max_
         _ptr(num_unique, torch.int32, "num_unique"), _ptr(workspace, None, "workspace"),
         0 if workspace is None else workspace.numel() * workspace.element_size(),
         _stream(stream)), "tc_cast_index")
+
+
+def tc_check_index(table_row_offset, num_tables, bags_per_table, total_rows, max_table_rows,
+                   indices, bag_offsets, num_pairs, report, stream=None) -> None:
+    _check(_lib.tc_check_index(
+        _ptr(table_row_offset, torch.int64, "table_row_offset"), num_tables, bags_per_table,
+        total_rows, max_table_rows, _ptr(indices, torch.int32, "indices"),
+        _ptr(bag_offsets, torch.int32, "bag_offsets"), num_pairs,
+        _ptr(report, torch.int64, "report"), _stream(stream)), "tc_check_index")
 
 
 def _ws(workspace):

@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(header):
 
 
 def test_version_and_status_strings(tc):
-    assert tc.tc_abi_version() == 4
+    assert tc.tc_abi_version() == 5
     lib = tc._lib
     for code, name in enumerate(["TC_OK", "TC_ERR_INVALID_ARG", "TC_ERR_UNSUPPORTED",
                                  "TC_ERR_WORKSPACE", "TC_ERR_HIP"]):
@@ -227,6 +227,27 @@ def test_backward_and_update_reject_bad_arguments(tc):
     assert coalesce(mu=-3) == tc.TC_ERR_INVALID_ARG
     assert coalesce(sp=None) == tc.TC_ERR_INVALID_ARG
     assert coalesce(mu=0) == tc.TC_OK
+    assert h.untouched()
+
+
+def test_check_index_rejects_bad_arguments(tc):
+    lib, h = tc._lib, HostBuffers()
+
+    def f(**k):
+        return lib.tc_check_index(k.get("off", h.lp()), k.get("T", 1), k.get("B", 50),
+                                  k.get("rows", 100), k.get("mtr", 0), k.get("idx", h.ip()),
+                                  k.get("bo", h.ip()), k.get("n", 1000), k.get("rep", h.lp()),
+                                  None)
+    assert f(rep=None) == tc.TC_ERR_INVALID_ARG and "null" in _err(tc)
+    assert f(rep=h.lp() + 4) == tc.TC_ERR_INVALID_ARG and "aligned" in _err(tc)
+    assert f(off=None) == tc.TC_ERR_INVALID_ARG
+    assert f(bo=None) == tc.TC_ERR_INVALID_ARG
+    assert f(idx=None) == tc.TC_ERR_INVALID_ARG
+    assert f(T=-1) == tc.TC_ERR_INVALID_ARG and "negative" in _err(tc)
+    assert f(mtr=-1) == tc.TC_ERR_INVALID_ARG
+    assert f(n=2 ** 31) == tc.TC_ERR_INVALID_ARG
+    assert f(rows=2 ** 31) == tc.TC_ERR_INVALID_ARG
+    assert f(T=2 ** 16, B=2 ** 15) == tc.TC_ERR_INVALID_ARG and "bags" in _err(tc)
     assert h.untouched()
 
 
