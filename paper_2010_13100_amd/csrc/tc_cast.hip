@@ -199,10 +199,20 @@ __device__ __forceinline__ uint64_t match_digit_n(uint32_t d, bool ok, int bits)
     return peers;
 }
 
+// Whether every item of the wavefront where ok holds has the same digit (a
+// run of one hot row, common in the later passes under skewed keys); *act
+// gets those lanes. Two ballots, against one per digit bit for a match.
+__device__ __forceinline__ bool all_same_digit(uint32_t d, bool ok, uint64_t *act) {
+    const uint32_t d0 = __builtin_amdgcn_readfirstlane(d);
+    *act = __ballot(ok);
+    return __ballot(ok && d == d0) == *act;
+}
+
 // ---------------------------------------------------------------------------
-// 2a. per-tile digit histogram -> counts[digit * tiles + tile]. Equal digits
-// within a wavefront are counted by one lane (no LDS atomic conflicts under
-// skewed keys). Blocks past the last tile write zeros.
+// 2a. per-tile digit histogram -> counts[digit * tiles + tile]. Every item
+// adds one to its wave's count of its digit (an LDS atomic; the order of
+// the adds does not matter here), except that a wavefront whose items share
+// one digit adds them all at once. Blocks past the last tile write zeros.
 template <int BITS>
 __global__ __launch_bounds__(kBlock) void k_radix_hist(const int32_t *__restrict__ keys,
                                                        int32_t n, int shift,
@@ -227,8 +237,12 @@ __global__ __launch_bounds__(kBlock) void k_radix_hist(const int32_t *__restrict
     for (int i = 0; i < kItems; ++i) {
         const bool ok = base + i * kWave + lane < tr.p1;
         const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
-        const uint64_t peers = match_digit<BITS>(d, ok);
-        if (ok && (peers & lanemask_lt(lane)) == 0) atomicAdd(&hist[w][d], __popcll(peers));
+        uint64_t act;
+        if (all_same_digit(d, ok, &act)) {
+            if (lane == 0 && act) atomicAdd(&hist[w][d], __popcll(act));
+        } else if (ok) {
+            atomicAdd(&hist[w][d], 1);
+        }
     }
     __syncthreads();
     for (int d = tid; d < R; d += kBlock) {
@@ -268,7 +282,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scan(int32_t *__restrict__ cou
 }
 
 // 2c. stable scatter of one tile. Within a wavefront the lanes holding equal
-// digits are found with ballots; the lowest of them adds their number to the
+// digits are found with ballots (two if they all share one digit); the lowest of them adds their number to the
 // wave's running count of that digit with one LDS atomic (the returned old
 // value is the count of that digit in earlier items, since a wave's LDS
 // operations complete in order) and the others take it from that lane. The
@@ -339,7 +353,8 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
     for (int i = 0; i < kItems; ++i) {
         const bool ok = base + i * kWave + lane < tr.p1;
         const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
-        const uint64_t peers = match_digit<BITS>(d, ok);
+        uint64_t act;
+        const uint64_t peers = all_same_digit(d, ok, &act) ? act : match_digit<BITS>(d, ok);
         const uint64_t lower = peers & lanemask_lt(lane);
         lower_n[i] = __popcll(lower);
         leader[i] = peers ? __builtin_ctzll(peers) : lane;
@@ -583,7 +598,9 @@ __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
             key[i] = ok ? keys[cur][j] : 0;
             val[i] = ok ? vals[cur][j] : 0;
             const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
-            const uint64_t peers = match_digit_n(d, ok, pbits);
+            uint64_t act;
+            const uint64_t peers =
+                all_same_digit(d, ok, &act) ? act : match_digit_n(d, ok, pbits);
             const uint64_t lower = peers & lanemask_lt(lane);
             lower_n[i] = __popcll(lower);
             leader[i] = peers ? __builtin_ctzll(peers) : lane;
