@@ -192,8 +192,8 @@ tc_status tc_embed_coalesce(const float *expanded, int64_t num_pairs, int32_t di
 /*
  * Bytes of a backward workspace that covers a step of up to num_pairs pairs
  * with rows of `dim` floats, for tc_embed_backward, tc_embed_backward_update
- * and tc_embed_coalesce; 0 if no segment can be long (num_pairs < 128) or
- * the arguments are out of range. About num_pairs * (dim / 256 + 0.15)
+ * and tc_embed_coalesce; 0 if no segment can be long (num_pairs < 80) or
+ * the arguments are out of range. About num_pairs * (dim / 256 + 0.25)
  * bytes.
  */
 size_t tc_backward_workspace_bytes(int64_t num_pairs, int32_t dim);

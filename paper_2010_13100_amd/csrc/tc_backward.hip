@@ -42,7 +42,7 @@ namespace tc {
 namespace {
 
 // Segments at least this long are long.
-constexpr int kLongSegment = 128;
+constexpr int kLongSegment = 80;
 // A long-segment workgroup: one consumer and kProducers producer wavefronts.
 constexpr int kProducers = 4;
 constexpr int kLongThreads = (1 + kProducers) * kWave;

@@ -47,13 +47,13 @@ def test_version_and_status_strings(tc):
 
 def test_backward_workspace_bytes(tc):
     f = tc.tc_backward_workspace_bytes
-    assert f(127, 64) == 0 and f(0, 64) == 0 and f(-5, 64) == 0 and f(128, 64) > 0
+    assert f(79, 64) == 0 and f(0, 64) == 0 and f(-5, 64) == 0 and f(80, 64) > 0
     assert f(10 ** 6, 0) == 0 and f(10 ** 6, 1028) == 0 and f(2 ** 31, 64) == 0
-    sizes = [f(n, 64) for n in (128, 2048, 4096, 10 ** 5, 10 ** 6, 10 ** 7)]
+    sizes = [f(n, 64) for n in (80, 2048, 4096, 10 ** 5, 10 ** 6, 10 ** 7)]
     assert sizes == sorted(sizes) and all(s % 256 == 0 for s in sizes)
     # piece sums (a row of dim floats per 1024 pairs) plus the work lists
     n = 10 ** 7
-    assert n // 1024 * 64 * 4 <= f(n, 64) <= n * (64 / 256 + 0.15)
+    assert n // 1024 * 64 * 4 <= f(n, 64) <= n * (64 / 256 + 0.25)
     assert f(10 ** 6, 256) > f(10 ** 6, 64)
 
 
