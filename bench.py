@@ -1,12 +1,14 @@
 """Benchmark one sparse-embedding training step on one MI355X.
 
-A step is the whole hot path on one synthetic batch: tc_embed_forward,
-tc_cast_index, then tc_embed_backward_update (the casted backward and the
-sparse update in one pass; --unfused calls tc_embed_backward and
-tc_sparse_update instead), back to back on one stream, with inputs already
-resident in HBM. Prints ONE JSON line.
+A step is the whole hot path on one synthetic batch: tc_embed_forward_cast
+(the forward gather-reduce and Tensor Casting in one call, overlapped), then
+tc_embed_backward_update (the casted backward and the sparse update in one
+pass), back to back on one stream, with inputs already resident in HBM.
+--no-overlap calls tc_embed_forward and tc_cast_index instead of the first;
+--unfused makes every step a separate call (tc_embed_forward, tc_cast_index,
+tc_embed_backward, tc_sparse_update). Prints ONE JSON line.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config c2] [--unfused]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config c2] [--no-overlap] [--unfused]
 
 Default workload: 8 tables x 1M rows x 64 fp32, batch 2048, 80 Zipf(1.05)
 indices per bag, SGD (configuration "c2"). Other configurations: c1..c5.
@@ -38,7 +40,7 @@ def algorithmic_bytes(w, n, u, nbags):
     # fused: the coalesced rows stay in registers (no G written, no G read)
     fused = n * 4 + (u + 1) * 4 + n * D4 + u * 4 + (rows_rw - 1) * u * D4
     return {"forward": fwd, "cast": cast, "backward": bwd, "update": upd,
-            "backward_update": fused}
+            "backward_update": fused, "forward_cast": fwd + cast}
 
 
 # Sources of each call's kernels, and the kernels one call launches.
@@ -47,7 +49,8 @@ KERNEL_SOURCES = {
     "backward": ["tc_internal.h", "tc_group_sum.h", "tc_optim.h", "tc_backward.hip"],
     "backward_update": ["tc_internal.h", "tc_group_sum.h", "tc_optim.h", "tc_backward.hip"],
     "update": ["tc_internal.h", "tc_optim.h", "tc_update.hip"],
-    "cast": ["tc_internal.h", "tc_cast.hip"],
+    "cast": ["tc_internal.h", "tc_group_sum.h", "tc_cast.hip"],
+    "forward_cast": ["tc_internal.h", "tc_group_sum.h", "tc_gather_reduce.hip", "tc_cast.hip"],
 }
 KERNEL_NAMES = {
     "forward": ["k_forward"],
@@ -57,7 +60,18 @@ KERNEL_NAMES = {
     "update": ["k_sparse_update"],
     "cast": ["k_cast_small", "k_build_keys", "k_radix_hist", "k_radix_scan", "k_radix_scatter",
              "k_seg_count", "k_seg_write"],
+    # the forward's bags run inside the scatters (or beside k_cast_small)
+    "forward_cast": ["k_cast_small", "k_build_keys", "k_radix_hist", "k_radix_scan",
+                     "k_radix_scatter", "k_seg_count", "k_seg_write", "k_forward"],
 }
+
+
+def step_calls(args, w):
+    """The library calls of one step, in order."""
+    rowwise = w.optimizer == "rowwise_adagrad"   # no fused backward + update for it
+    first = ["forward", "cast"] if (args.unfused or args.no_overlap) else ["forward_cast"]
+    last = ["backward", "update"] if (args.unfused or rowwise) else ["backward_update"]
+    return first + last
 
 
 def source_sha(call: str) -> str:
@@ -247,16 +261,16 @@ def setup(w, dev):
     return batches, trainer, dbat
 
 
-def measure_step(args, w, cfg_name, trainer, dbat, stream, unfused, traffic_key):
-    """Time args.steps steps (after args.warmup) and return the result line
-    (without cpu_baseline)."""
+def measure_step(args, w, cfg_name, trainer, dbat, stream, calls, traffic_key):
+    """Time args.steps steps (after args.warmup) of the given calls and
+    return the result line (without cpu_baseline)."""
     import numpy as np
     import torch
 
-    calls = (["forward", "cast", "backward", "update"] if unfused
-             else ["forward", "cast", "backward_update"])
     fns = {"forward": lambda d: trainer.forward(d["off"], d["idx"], d["bo"], stream),
            "cast": lambda d: trainer.cast(d["off"], d["idx"], d["bo"], d["n"], stream),
+           "forward_cast": lambda d: trainer.forward_cast(d["off"], d["idx"], d["bo"], d["n"],
+                                                          stream),
            "backward": lambda d: trainer.backward(d["grad"], stream),
            "update": lambda d: trainer.update(stream),
            "backward_update": lambda d: trainer.backward_update(d["grad"], stream)}
@@ -286,7 +300,9 @@ def measure_step(args, w, cfg_name, trainer, dbat, stream, unfused, traffic_key)
     skip = 1 if args.warmup > 1 else 0   # the first step also pays one-time costs
     per_call_ms = {c: float(np.mean([e[c][0].elapsed_time(e[c][1]) for e in wev[skip:]]))
                    for c in calls} if args.warmup else {c: float("nan") for c in calls}
-    single = [c for c in calls if c != "cast"]
+    # the dominant call among those with a bandwidth roofline (the cast's
+    # sort is bound by latency and arithmetic, not by HBM)
+    single = [c for c in calls if c not in ("cast", "forward_cast")]
     dom = max(single, key=lambda c: per_call_ms[c]) if args.warmup else single[-1]
 
     # timed steps: start/stop around the whole region, one event pair around
@@ -379,8 +395,7 @@ def run_sweep(args, base, cfg_name, dev):
         w = wl.variant(base, **{what: v})
         _, trainer, dbat = setup(w, dev)
         stream = torch.cuda.current_stream(dev)
-        unfused = args.unfused or w.optimizer == "rowwise_adagrad"
-        res = measure_step(args, w, cfg_name, trainer, dbat, stream, unfused, None)
+        res = measure_step(args, w, cfg_name, trainer, dbat, stream, step_calls(args, w), None)
         ab = run_ab(args, w, trainer, dbat, stream)
         print(json.dumps({
             "sweep": what, what: v, "workload": w.name,
@@ -411,7 +426,10 @@ def main():
                     help="instead of the step: time the paper's baseline backward "
                          "(expand-coalesce) against the casted backward and exit")
     ap.add_argument("--unfused", action="store_true",
-                    help="backward and update as two calls (tc_embed_backward, tc_sparse_update)")
+                    help="every step a call of its own: tc_embed_forward, tc_cast_index, "
+                         "tc_embed_backward, tc_sparse_update")
+    ap.add_argument("--no-overlap", action="store_true",
+                    help="forward and cast as two calls (tc_embed_forward, tc_cast_index)")
     ap.add_argument("--optimizer", default=None,
                     choices=["sgd", "adagrad", "rmsprop", "rowwise_adagrad"],
                     help="replace the workload's optimizer (row-wise Adagrad runs unfused)")
@@ -464,8 +482,8 @@ def main():
     if args.ab:
         print(json.dumps(run_ab(args, w, trainer, dbat, stream)), flush=True)
         return
-    unfused = args.unfused or w.optimizer == "rowwise_adagrad"
-    result = measure_step(args, w, args.config, trainer, dbat, stream, unfused, traffic_key)
+    result = measure_step(args, w, args.config, trainer, dbat, stream, step_calls(args, w),
+                          traffic_key)
     if args.cpu_budget > 0:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, batches[0], args.cpu_budget)

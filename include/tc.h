@@ -8,6 +8,8 @@
  *
  *   tc_embed_forward   embedding gather-reduce (Sec. II-B): pooled row sums
  *   tc_cast_index      Tensor Casting (Algorithm 2, Sec. IV-A)
+ *                      (tc_embed_forward_cast does these two in one call,
+ *                      overlapped, as the paper's runtime does, Sec. IV-B)
  *   tc_embed_backward  casted gradient gather-reduce (Algorithm 3)
  *   tc_sparse_update   gradient scatter with SGD, Adagrad (Eq. 2) or RMSprop
  *                      (Eq. 1), Sec. II-B
@@ -79,7 +81,7 @@
 extern "C" {
 #endif
 
-#define TC_ABI_VERSION 5
+#define TC_ABI_VERSION 6
 
 /* Segments at least this long are summed in pieces when a backward
  * workspace covers them (tc_embed_backward). */
@@ -151,6 +153,29 @@ tc_status tc_cast_index(const int64_t *table_row_offset, int32_t num_tables,
                         int32_t *seg_offsets, int32_t *casted_src, int32_t *casted_dst,
                         int32_t *num_unique, void *workspace, size_t workspace_bytes,
                         hipStream_t stream);
+
+/*
+ * tc_embed_forward followed by tc_cast_index in one call, with the same
+ * results bit for bit, the forward overlapped with the cast: casting needs
+ * only the index array, so it can run while the forward gather-reduce reads
+ * the table (the paper's runtime hides the casting latency inside forward
+ * propagation, Sec. IV-B). For dim in [36, 256] the forward runs in the
+ * cast's own launches: beside the single-workgroup cast of a small batch
+ * (up to 8192 pairs), else in the launch that builds the cast's (row, bag)
+ * pairs from the same index array; for other dims the forward runs first,
+ * then the cast. Arguments are those of the two calls (max_table_rows
+ * and the workspace as for tc_cast_index, W and out as for
+ * tc_embed_forward); out must not overlap the cast's outputs or workspace.
+ * Every argument is checked before anything is launched.
+ */
+tc_status tc_embed_forward_cast(const float *W, int64_t total_rows, int32_t dim,
+                                const int64_t *table_row_offset, int32_t num_tables,
+                                int32_t bags_per_table, int64_t max_table_rows,
+                                const int32_t *indices, const int32_t *bag_offsets,
+                                int64_t num_pairs, float *out, int32_t *unique_rows,
+                                int32_t *seg_offsets, int32_t *casted_src, int32_t *casted_dst,
+                                int32_t *num_unique, void *workspace, size_t workspace_bytes,
+                                hipStream_t stream);
 
 /*
  * Stable argsort of the pairs by row (Algorithm 1's ArgSort, Sec. II-B):

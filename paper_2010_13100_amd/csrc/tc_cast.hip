@@ -37,7 +37,7 @@
 // walks them 64 at a time, lane l taking position base + 64*i + l, so tile
 // order = (wave, iteration, lane) order and every pass is stable. No atomics
 // on global memory; nothing here depends on scheduling order.
-#include "tc_internal.h"
+#include "tc_group_sum.h"
 
 namespace tc {
 namespace {
@@ -89,62 +89,73 @@ struct alignas(16) TileRec {
     int32_t p0, p1, first, next, pstart, rowoff, s, pad;
 };
 // ---------------------------------------------------------------------------
-// 1. key build: one group of 16 lanes per bag writes that bag's pairs; keys
-// are table-local rows when `local`, else global rows; values are bag ids
-// (dst), or pair positions when `positions` (an argsort). With `local`, block
-// 0 also writes the tile records of the num_tables segments.
-__global__ __launch_bounds__(kBlock) void k_build_keys(
-    const int32_t *__restrict__ indices, const int32_t *__restrict__ bag_offsets,
-    const int64_t *__restrict__ table_row_offset, int64_t num_bags, int32_t bags_per_table,
-    int32_t num_tables, bool local, bool positions, TileRec *__restrict__ tiles,
-    int32_t num_tile_slots, int32_t *__restrict__ keys, int32_t *__restrict__ vals) {
-    if (local && blockIdx.x == 0) {
-        __shared__ int32_t tstart[kMaxSegTables + 1], pstart[kMaxSegTables + 1];
-        __shared__ int32_t rowoff[kMaxSegTables];
-        const int t = threadIdx.x;
-        int32_t p0 = 0, n_t = 0;
-        if (t < num_tables) {
-            p0 = bag_offsets[int64_t(t) * bags_per_table];
-            n_t = bag_offsets[int64_t(t + 1) * bags_per_table] - p0;
-            rowoff[t] = int32_t(table_row_offset[t]);
-        }
-        int32_t total;
-        const int32_t ts = block_exclusive_scan((n_t + kTile - 1) / kTile, &total);
-        if (t < num_tables) {
-            tstart[t] = ts;
-            pstart[t] = p0;
-        }
-        if (t == 0) {
-            tstart[num_tables] = total;
-            pstart[num_tables] = bag_offsets[num_bags];
-        }
-        __syncthreads();
-        for (int32_t b = t; b < num_tile_slots; b += kBlock) {
-            TileRec r{0, 0, 0, 0, 0, 0, -1, 0};
-            if (b < total) {
-                // the segment holding tile b: last s with tstart[s] <= b
-                // (segments without pairs have no tiles and are passed over)
-                int32_t lo = 0, hi = num_tables - 1;
-                while (lo < hi) {
-                    const int32_t mid = (lo + hi + 1) / 2;
-                    if (tstart[mid] <= b) lo = mid; else hi = mid - 1;
-                }
-                const int32_t sg = lo;
-                r.s = sg;
-                r.first = tstart[sg];
-                r.next = tstart[sg + 1];
-                r.pstart = pstart[sg];
-                r.rowoff = rowoff[sg];
-                r.p0 = pstart[sg] + (b - r.first) * kTile;
-                const int32_t end = pstart[sg + 1];
-                r.p1 = r.p0 + kTile < end ? r.p0 + kTile : end;
-            }
-            tiles[b] = r;
-        }
+// 1. key build. The tile records of the num_tables segments (table-local
+// sort), written by one whole workgroup.
+__device__ void write_tile_records(const int32_t *__restrict__ bag_offsets,
+                                   const int64_t *__restrict__ table_row_offset,
+                                   int64_t num_bags, int32_t bags_per_table, int32_t num_tables,
+                                   TileRec *__restrict__ tiles, int32_t num_tile_slots) {
+    __shared__ int32_t tstart[kMaxSegTables + 1], pstart[kMaxSegTables + 1];
+    __shared__ int32_t rowoff[kMaxSegTables];
+    const int t = threadIdx.x;
+    int32_t p0 = 0, n_t = 0;
+    if (t < num_tables) {
+        p0 = bag_offsets[int64_t(t) * bags_per_table];
+        n_t = bag_offsets[int64_t(t + 1) * bags_per_table] - p0;
+        rowoff[t] = int32_t(table_row_offset[t]);
     }
+    int32_t total;
+    const int32_t ts = block_exclusive_scan((n_t + kTile - 1) / kTile, &total);
+    if (t < num_tables) {
+        tstart[t] = ts;
+        pstart[t] = p0;
+    }
+    if (t == 0) {
+        tstart[num_tables] = total;
+        pstart[num_tables] = bag_offsets[num_bags];
+    }
+    __syncthreads();
+    for (int32_t b = t; b < num_tile_slots; b += kBlock) {
+        TileRec r{0, 0, 0, 0, 0, 0, -1, 0};
+        if (b < total) {
+            // the segment holding tile b: last s with tstart[s] <= b
+            // (segments without pairs have no tiles and are passed over)
+            int32_t lo = 0, hi = num_tables - 1;
+            while (lo < hi) {
+                const int32_t mid = (lo + hi + 1) / 2;
+                if (tstart[mid] <= b) lo = mid; else hi = mid - 1;
+            }
+            const int32_t sg = lo;
+            r.s = sg;
+            r.first = tstart[sg];
+            r.next = tstart[sg + 1];
+            r.pstart = pstart[sg];
+            r.rowoff = rowoff[sg];
+            r.p0 = pstart[sg] + (b - r.first) * kTile;
+            const int32_t end = pstart[sg + 1];
+            r.p1 = r.p0 + kTile < end ? r.p0 + kTile : end;
+        }
+        tiles[b] = r;
+    }
+}
+
+// (src, dst) pairs: one group of 16 lanes per bag writes that bag's pairs;
+// keys are table-local rows when `local`, else global rows; values are bag
+// ids (dst), or pair positions when `positions` (an argsort). Workgroup
+// `block` of `nblocks` takes every nblocks-th run of bags; with `local`,
+// block 0 also writes the tile records of the num_tables segments.
+__device__ __forceinline__ void build_pairs(
+    int64_t block, int64_t nblocks, const int32_t *__restrict__ indices,
+    const int32_t *__restrict__ bag_offsets, const int64_t *__restrict__ table_row_offset,
+    int64_t num_bags, int32_t bags_per_table, int32_t num_tables, bool local, bool positions,
+    TileRec *__restrict__ tiles, int32_t num_tile_slots, int32_t *__restrict__ keys,
+    int32_t *__restrict__ vals) {
+    if (local && block == 0)
+        write_tile_records(bag_offsets, table_row_offset, num_bags, bags_per_table, num_tables,
+                           tiles, num_tile_slots);
     constexpr int kLanes = 16;
-    const int64_t group = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / kLanes;
-    const int64_t ngroups = (int64_t(gridDim.x) * blockDim.x) / kLanes;
+    const int64_t group = (block * kBlock + threadIdx.x) / kLanes;
+    const int64_t ngroups = (nblocks * kBlock) / kLanes;
     const int sub = threadIdx.x & (kLanes - 1);
     for (int64_t g = group; g < num_bags; g += ngroups) {
         const int32_t beg = bag_offsets[g], end = bag_offsets[g + 1];
@@ -154,6 +165,38 @@ __global__ __launch_bounds__(kBlock) void k_build_keys(
             vals[j] = positions ? j : int32_t(g);
         }
     }
+}
+
+__global__ __launch_bounds__(kBlock) void k_build_keys(
+    const int32_t *__restrict__ indices, const int32_t *__restrict__ bag_offsets,
+    const int64_t *__restrict__ table_row_offset, int64_t num_bags, int32_t bags_per_table,
+    int32_t num_tables, bool local, bool positions, TileRec *__restrict__ tiles,
+    int32_t num_tile_slots, int32_t *__restrict__ keys, int32_t *__restrict__ vals) {
+    build_pairs(blockIdx.x, gridDim.x, indices, bag_offsets, table_row_offset, num_bags,
+                bags_per_table, num_tables, local, positions, tiles, num_tile_slots, keys, vals);
+}
+
+// The key build and the forward gather-reduce in one launch
+// (tc_embed_forward_cast): the first build_blocks workgroups build the pairs
+// as k_build_keys does, the others run the forward (FL lanes per bag, as
+// k_forward). Both read the index array; kept in separate workgroups, the
+// pair stores stay out of the forward's chains of dependent loads.
+template <int FL>
+__global__ __launch_bounds__(kBlock) void k_forward_keys(FwdSlice f, int32_t build_blocks,
+                                                         int32_t num_tables, bool local,
+                                                         TileRec *__restrict__ tiles,
+                                                         int32_t num_tile_slots,
+                                                         int32_t *__restrict__ keys,
+                                                         int32_t *__restrict__ vals) {
+    if (int32_t(blockIdx.x) < build_blocks) {  // uniform
+        build_pairs(blockIdx.x, build_blocks, f.ids, f.offsets, f.table_row_offset, f.bag_hi,
+                    f.bags_per_table, num_tables, local, false, tiles, num_tile_slots, keys,
+                    vals);
+        return;
+    }
+    constexpr int64_t kWaves = kBlock / kWave;
+    forward_bags<FL, 1>(f, (int64_t(blockIdx.x) - build_blocks) * kWaves + threadIdx.x / kWave,
+                        (int64_t(gridDim.x) - build_blocks) * kWaves);
 }
 
 // This block's tile: its record (table-local sort) or a plain slice of the
@@ -538,15 +581,28 @@ __device__ __forceinline__ int32_t small_block_scan(int32_t v, int32_t *total) {
     return wbase + incl - v;
 }
 
+//
+// With FL > 0 (tc_embed_forward_cast) the workgroups after the first run the
+// forward gather-reduce beside it, FL lanes per bag: a small cast keeps one
+// CU busy and leaves the others to the forward.
+template <int FL>
 __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
     const int32_t *__restrict__ indices, const int32_t *__restrict__ bag_offsets,
     const int64_t *__restrict__ table_row_offset, int32_t num_tables, int32_t num_bags,
     int32_t bags_per_table, int32_t n, int bits, bool positions, int32_t *__restrict__ unique_rows,
     int32_t *__restrict__ seg_offsets, int32_t *__restrict__ casted_src,
-    int32_t *__restrict__ casted_dst, int32_t *__restrict__ num_unique) {
+    int32_t *__restrict__ casted_dst, int32_t *__restrict__ num_unique, FwdSlice fs) {
     __shared__ int32_t keys[2][kSmallPairs];
     __shared__ int32_t vals[2][kSmallPairs];
     __shared__ int32_t wcount[kSmallWaves][kMaxRadix];
+    if constexpr (FL > 0) {
+        if (blockIdx.x > 0) {  // uniform: a forward workgroup
+            constexpr int64_t kWaves = kSmallThreads / kWave;
+            forward_bags<FL, 1>(fs, (int64_t(blockIdx.x) - 1) * kWaves + threadIdx.x / kWave,
+                                (int64_t(gridDim.x) - 1) * kWaves);
+            return;
+        }
+    }
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
 
     // (src, dst) pairs from the bag-major CSR index: 16 lanes per bag. The
@@ -767,15 +823,25 @@ extern "C" size_t tc_cast_workspace_bytes(int64_t num_pairs, int64_t total_rows,
 }
 
 namespace {
+// The forward over all bags of fwd as its own kernel.
+tc_status forward_alone(const FwdSlice &fwd, hipStream_t stream) {
+    return launch_forward(fwd.W, fwd.dim, fwd.ids, fwd.offsets, fwd.table_row_offset,
+                          fwd.bags_per_table, fwd.bag_hi, fwd.out, stream);
+}
+
 // The sort and segment build behind tc_cast_index (values = bag ids) and
 // tc_argsort_rows (values = pair positions). `what` names the entry point in
-// error messages.
+// error messages. With fwd (tc_embed_forward_cast; values = bag ids), the
+// forward gather-reduce of all fwd->bag_hi bags runs too: beside the
+// single-workgroup cast, or as the key-building kernel of the radix sort,
+// or, for row shapes without such kernels, as its own kernel first.
 tc_status cast_impl(const char *what, bool positions, const int64_t *table_row_offset,
                     int32_t num_tables, int32_t bags_per_table, int64_t total_rows,
                     int64_t max_table_rows, const int32_t *indices, const int32_t *bag_offsets,
                     int64_t num_pairs, int32_t *unique_rows, int32_t *seg_offsets,
                     int32_t *casted_src, int32_t *casted_dst, int32_t *num_unique,
-                    void *workspace, size_t workspace_bytes, hipStream_t stream) {
+                    void *workspace, size_t workspace_bytes, hipStream_t stream,
+                    const FwdSlice *fwd = nullptr) {
     TC_REQUIRE(num_tables >= 0 && bags_per_table >= 0 && total_rows >= 0 && num_pairs >= 0 &&
                    max_table_rows >= 0,
                TC_ERR_INVALID_ARG, "%s: negative size", what);
@@ -786,6 +852,10 @@ tc_status cast_impl(const char *what, bool positions, const int64_t *table_row_o
                "%s: more than 2^31-1 bags", what);
     TC_REQUIRE(seg_offsets && num_unique, TC_ERR_INVALID_ARG, "%s: null pointer", what);
     if (num_pairs == 0) {
+        if (fwd) {
+            const tc_status st = forward_alone(*fwd, stream);
+            if (st != TC_OK) return st;
+        }
         k_cast_empty<<<1, kWave, 0, stream>>>(seg_offsets, num_unique);
         return check_launch("k_cast_empty");
     }
@@ -801,12 +871,31 @@ tc_status cast_impl(const char *what, bool positions, const int64_t *table_row_o
     TC_REQUIRE(plan.sort_tiles < (int64_t(1) << 31) / kMaxRadix, TC_ERR_INVALID_ARG,
                "%s: too many pairs", what);
 
+    const int fl = fwd ? ride_along_lanes(fwd->dim) : 0;
+    if (fwd && fl == 0) {
+        const tc_status st = forward_alone(*fwd, stream);
+        if (st != TC_OK) return st;
+    }
     if (num_pairs <= kSmallPairs) {
-        // one workgroup in LDS (the workspace is not touched)
-        k_cast_small<<<1, kSmallThreads, 0, stream>>>(
-            indices, bag_offsets, table_row_offset, num_tables, int32_t(num_bags), bags_per_table,
-            int32_t(num_pairs), key_bits(total_rows), positions, unique_rows, seg_offsets,
-            casted_src, casted_dst, num_unique);
+        // one workgroup in LDS (the workspace is not touched); the forward's
+        // workgroups, if any, run beside it (one per CU at most: each holds
+        // the kernel's LDS), one bag per lane group
+        unsigned fb = 0;
+        if (fl) {
+            const int64_t per_block = int64_t(kSmallThreads / kWave) * (kWave / fl);
+            fb = grid_for(num_bags, per_block, kNumCUs - 1);
+        }
+        const FwdSlice fs = fl ? *fwd : FwdSlice{};
+#define TC_SMALL(FL)                                                                         \
+    k_cast_small<FL><<<1 + fb, kSmallThreads, 0, stream>>>(                                  \
+        indices, bag_offsets, table_row_offset, num_tables, int32_t(num_bags), bags_per_table, \
+        int32_t(num_pairs), key_bits(total_rows), positions, unique_rows, seg_offsets,        \
+        casted_src, casted_dst, num_unique, fs)
+        if (fl == 16) TC_SMALL(16);
+        else if (fl == 32) TC_SMALL(32);
+        else if (fl == 64) TC_SMALL(64);
+        else TC_SMALL(0);
+#undef TC_SMALL
         return check_launch("k_cast_small");
     }
     // Table-local keys when the tables are known to be small enough to save
@@ -828,7 +917,21 @@ tc_status cast_impl(const char *what, bool positions, const int64_t *table_row_o
     const int32_t sort_tiles = int32_t(plan.sort_tiles);
     const int32_t seg_tiles = int32_t(plan.seg_tiles);
 
-    {
+    if (fl) {
+        // the key build's workgroups, then the forward's, in one launch
+        const unsigned bb = grid_for(num_bags, kBlock / 16, int64_t(kNumCUs) * 8);
+        const int64_t per_block = int64_t(kBlock / kWave) * (kWave / fl);
+        const unsigned grid = bb + grid_for(num_bags, per_block, int64_t(kNumCUs) * 32);
+#define TC_FWD_KEYS(FL)                                                                      \
+    k_forward_keys<FL><<<grid, kBlock, 0, stream>>>(*fwd, int32_t(bb), num_tables, local,      \
+                                                    recs, sort_tiles, ka, va)
+        if (fl == 16) TC_FWD_KEYS(16);
+        else if (fl == 32) TC_FWD_KEYS(32);
+        else TC_FWD_KEYS(64);
+#undef TC_FWD_KEYS
+        tc_status st = check_launch("k_forward_keys");
+        if (st != TC_OK) return st;
+    } else {
         const unsigned grid = grid_for(num_bags, kBlock / 16, int64_t(kNumCUs) * 8);
         k_build_keys<<<grid, kBlock, 0, stream>>>(indices, bag_offsets, table_row_offset,
                                                   num_bags, bags_per_table, num_tables, local,
@@ -878,6 +981,34 @@ extern "C" tc_status tc_cast_index(const int64_t *table_row_offset, int32_t num_
                      total_rows, max_table_rows, indices, bag_offsets, num_pairs, unique_rows,
                      seg_offsets, casted_src, casted_dst, num_unique, workspace,
                      workspace_bytes, stream);
+}
+
+extern "C" tc_status tc_embed_forward_cast(
+    const float *W, int64_t total_rows, int32_t dim, const int64_t *table_row_offset,
+    int32_t num_tables, int32_t bags_per_table, int64_t max_table_rows, const int32_t *indices,
+    const int32_t *bag_offsets, int64_t num_pairs, float *out, int32_t *unique_rows,
+    int32_t *seg_offsets, int32_t *casted_src, int32_t *casted_dst, int32_t *num_unique,
+    void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    clear_error();
+    const char *what = "tc_embed_forward_cast";
+    TC_REQUIRE(num_tables >= 0 && bags_per_table >= 0, TC_ERR_INVALID_ARG, "%s: negative size",
+               what);
+    TC_REQUIRE(dim > 0 && dim % 4 == 0 && dim <= kMaxDim, TC_ERR_UNSUPPORTED,
+               "%s: dim %d must be a multiple of 4 in [4, %d]", what, dim, kMaxDim);
+    const int64_t num_bags = int64_t(num_tables) * bags_per_table;
+    if (num_bags > 0) {
+        TC_REQUIRE(W && out && table_row_offset && bag_offsets, TC_ERR_INVALID_ARG,
+                   "%s: null pointer", what);
+        TC_REQUIRE(aligned16(W) && aligned16(out), TC_ERR_UNSUPPORTED,
+                   "%s: W and out must be 16-byte aligned", what);
+    }
+    // the cast checks the rest before anything is launched
+    const FwdSlice f{W, indices, bag_offsets, table_row_offset, out, 0, num_bags, dim,
+                     bags_per_table};
+    return cast_impl(what, false, table_row_offset, num_tables, bags_per_table, total_rows,
+                     max_table_rows, indices, bag_offsets, num_pairs, unique_rows, seg_offsets,
+                     casted_src, casted_dst, num_unique, workspace, workspace_bytes, stream,
+                     num_bags > 0 ? &f : nullptr);
 }
 
 extern "C" tc_status tc_argsort_rows(const int64_t *table_row_offset, int32_t num_tables,

@@ -23,33 +23,13 @@ namespace {
 
 // Forward: one output row per bag, source row = table_row_offset[bag / B] + ids[j].
 template <int LANES, int CHUNKS>
-__global__ __launch_bounds__(kBlock) void k_forward(
-    const float *__restrict__ W, int32_t dim, const int32_t *__restrict__ ids,
-    const int32_t *__restrict__ offsets, const int64_t *__restrict__ table_row_offset,
-    int32_t bags_per_table, int64_t num_bags, float *__restrict__ out) {
-    constexpr int kGroups = kWave / LANES;  // bags per wavefront
-    const int lane = threadIdx.x & (kWave - 1);
-    const int sub = lane & (LANES - 1);
-    const int grp = lane / LANES;
+__global__ __launch_bounds__(kBlock) void k_forward(FwdSlice f) {
     const int64_t wave = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / kWave;
     const int64_t nwave = (int64_t(gridDim.x) * blockDim.x) / kWave;
-    for (int64_t o0 = wave * kGroups; o0 < num_bags; o0 += nwave * kGroups) {
-        const int64_t o = o0 + grp;
-        const bool live = o < num_bags;
-        int32_t beg = 0, end = 0;
-        int64_t base = 0;
-        if (live) {
-            beg = offsets[o];
-            end = offsets[o + 1];
-            base = table_row_offset[o / bags_per_table];
-        }
-        float4 acc[CHUNKS];
-#pragma unroll
-        for (int c = 0; c < CHUNKS; ++c) acc[c] = make_float4(0.f, 0.f, 0.f, 0.f);
-        group_range_sum<LANES, CHUNKS>(W, dim, ids, base, beg, end, sub, acc);
-        if (live) group_store<LANES, CHUNKS>(out + o * int64_t(dim), dim, sub, acc);
-    }
+    forward_bags<LANES, CHUNKS>(f, wave, nwave);
 }
+
+}  // namespace
 
 tc_status launch_forward(const float *W, int32_t dim, const int32_t *ids, const int32_t *offsets,
                          const int64_t *table_row_offset, int32_t bags_per_table,
@@ -59,10 +39,10 @@ tc_status launch_forward(const float *W, int32_t dim, const int32_t *ids, const 
     // up to 32 workgroups per CU in the grid (8 are resident at a time): on
     // 33 GB tables the random row reads finish about 3% sooner than with 8
     const unsigned grid = grid_for(num_bags, rows_per_block, int64_t(kNumCUs) * 32);
+    const FwdSlice f{W, ids, offsets, table_row_offset, out, 0, num_bags, dim, bags_per_table};
 #define TC_FWD_CASE(L, C)                                                                      \
     if (s.lanes == L && s.chunks == C) {                                                       \
-        k_forward<L, C><<<grid, kBlock, 0, stream>>>(W, dim, ids, offsets, table_row_offset,    \
-                                                     bags_per_table, num_bags, out);            \
+        k_forward<L, C><<<grid, kBlock, 0, stream>>>(f);                                       \
         return check_launch("k_forward");                                                      \
     }
     TC_FWD_CASE(1, 1)
@@ -80,7 +60,6 @@ tc_status launch_forward(const float *W, int32_t dim, const int32_t *ids, const 
     return TC_ERR_UNSUPPORTED;
 }
 
-}  // namespace
 }  // namespace tc
 
 using namespace tc;

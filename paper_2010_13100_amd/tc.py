@@ -28,6 +28,8 @@ _SIGNATURES = {
     "tc_cast_workspace_bytes": (_sz, [_i64, _i64, _i32]),
     "tc_cast_index": (_i32, [_vp, _i32, _i32, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp,
                              _vp, _vp, _sz, _vp]),
+    "tc_embed_forward_cast": (_i32, [_vp, _i64, _i32, _vp, _i32, _i32, _i64, _vp, _vp, _i64,
+                                     _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "tc_embed_backward": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _i64, _vp, _vp, _sz, _vp]),
     "tc_backward_workspace_bytes": (_sz, [_i64, _i32]),
     "tc_sparse_update": (_i32, [_vp, _vp, _i64, _i32, _vp, _vp, _vp, _i64, _i32, _f32, _f32,
@@ -119,6 +121,20 @@ def tc_cast_index(table_row_offset, num_tables, bags_per_table, total_rows, max_
         _ptr(num_unique, torch.int32, "num_unique"), _ptr(workspace, None, "workspace"),
         0 if workspace is None else workspace.numel() * workspace.element_size(),
         _stream(stream)), "tc_cast_index")
+
+
+def tc_embed_forward_cast(W, table_row_offset, num_tables, bags_per_table, max_table_rows,
+                          indices, bag_offsets, num_pairs, out, unique_rows, seg_offsets,
+                          casted_src, casted_dst, num_unique, workspace, stream=None) -> None:
+    _check(_lib.tc_embed_forward_cast(
+        _ptr(W, torch.float32, "W"), W.shape[0], W.shape[1],
+        _ptr(table_row_offset, torch.int64, "table_row_offset"), num_tables, bags_per_table,
+        max_table_rows, _ptr(indices, torch.int32, "indices"),
+        _ptr(bag_offsets, torch.int32, "bag_offsets"), num_pairs,
+        _ptr(out, torch.float32, "out"), _ptr(unique_rows, torch.int32, "unique_rows"),
+        _ptr(seg_offsets, torch.int32, "seg_offsets"), _ptr(casted_src, torch.int32, "casted_src"),
+        _ptr(casted_dst, torch.int32, "casted_dst"), _ptr(num_unique, torch.int32, "num_unique"),
+        *_ws(workspace), _stream(stream)), "tc_embed_forward_cast")
 
 
 def tc_check_index(table_row_offset, num_tables, bags_per_table, total_rows, max_table_rows,
@@ -256,6 +272,15 @@ class EmbeddingTrainer:
                       self.seg_offsets, self.casted_src, self.casted_dst if with_casted_dst else None,
                       self.num_unique, self.workspace, stream)
 
+    def forward_cast(self, table_row_offset, indices, bag_offsets, num_pairs, stream=None,
+                     with_casted_dst=False):
+        """forward + cast in one call, overlapped (same results as the two)."""
+        tc_embed_forward_cast(self.W, table_row_offset, self.num_tables, self.bags_per_table,
+                              self.max_table_rows, indices, bag_offsets, num_pairs, self.out,
+                              self.unique_rows, self.seg_offsets, self.casted_src,
+                              self.casted_dst if with_casted_dst else None, self.num_unique,
+                              self.workspace, stream)
+
     def backward(self, grad_out, stream=None):
         tc_embed_backward(grad_out, self.seg_offsets, self.casted_src, self.num_unique,
                           self.max_unique, self.coal, self.bwd_workspace, stream)
@@ -292,9 +317,13 @@ class EmbeddingTrainer:
     def step(self, table_row_offset, indices, bag_offsets, num_pairs, grad_out, stream=None,
              fused=True):
         """forward + cast + backward + update, stream-ordered; with fused the
-        last two are one call (row-wise Adagrad always takes the two calls)."""
-        self.forward(table_row_offset, indices, bag_offsets, stream)
-        self.cast(table_row_offset, indices, bag_offsets, num_pairs, stream)
+        first two are one overlapped call and the last two one pass
+        (row-wise Adagrad always takes the backward and update calls)."""
+        if fused:
+            self.forward_cast(table_row_offset, indices, bag_offsets, num_pairs, stream)
+        else:
+            self.forward(table_row_offset, indices, bag_offsets, stream)
+            self.cast(table_row_offset, indices, bag_offsets, num_pairs, stream)
         if fused and self.opt_kind != TC_OPT_ROWWISE_ADAGRAD:
             self.backward_update(grad_out, stream)
         else:

@@ -68,14 +68,19 @@ class GpuRun:
             device_fill.fill_uniform(self.trainer.W, seed=0, lo=w.init_lo, hi=w.init_hi)
 
     def run_step(self, b: wl.Batch, with_casted_dst=True, fused=False, store_coal=True):
-        """The four calls on the current stream (with fused, backward and
-        update as one tc_embed_backward_update call, storing the coalesced
-        rows if store_coal); outputs stay on the GPU."""
+        """The step's calls on the current stream; outputs stay on the GPU.
+        fused: the step as the benchmark runs it, forward and cast as one
+        tc_embed_forward_cast call and backward and update as one
+        tc_embed_backward_update call (storing the coalesced rows if
+        store_coal); else the four calls one by one."""
         t = self.trainer
         off, idx, bo = to_dev(b.table_row_offset), to_dev(b.indices), to_dev(b.bag_offsets)
         g = to_dev(b.grad_out)
-        t.forward(off, idx, bo)
-        t.cast(off, idx, bo, b.num_pairs, with_casted_dst=with_casted_dst)
+        if fused:
+            t.forward_cast(off, idx, bo, b.num_pairs, with_casted_dst=with_casted_dst)
+        else:
+            t.forward(off, idx, bo)
+            t.cast(off, idx, bo, b.num_pairs, with_casted_dst=with_casted_dst)
         if fused:
             t.backward_update(g, store_coal=store_coal)
         else:

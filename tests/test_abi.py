@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(header):
 
 
 def test_version_and_status_strings(tc):
-    assert tc.tc_abi_version() == 5
+    assert tc.tc_abi_version() == 6
     lib = tc._lib
     for code, name in enumerate(["TC_OK", "TC_ERR_INVALID_ARG", "TC_ERR_UNSUPPORTED",
                                  "TC_ERR_WORKSPACE", "TC_ERR_HIP"]):
@@ -227,6 +227,32 @@ def test_backward_and_update_reject_bad_arguments(tc):
     assert coalesce(mu=-3) == tc.TC_ERR_INVALID_ARG
     assert coalesce(sp=None) == tc.TC_ERR_INVALID_ARG
     assert coalesce(mu=0) == tc.TC_OK
+    assert h.untouched()
+
+
+def test_forward_cast_rejects_bad_arguments(tc):
+    lib, h = tc._lib, HostBuffers()
+    need = lib.tc_cast_workspace_bytes(1000, 100, 1)
+
+    def f(**k):
+        return lib.tc_embed_forward_cast(
+            k.get("W", h.fp()), k.get("rows", 100), k.get("dim", 64), k.get("off", h.lp()),
+            k.get("T", 1), k.get("B", 50), k.get("mtr", 100), k.get("idx", h.ip()),
+            k.get("bo", h.ip()), k.get("n", 1000), k.get("out", h.fp()), k.get("ur", h.ip()),
+            k.get("so", h.ip()), k.get("cs", h.ip()), None, k.get("nu", h.ip()),
+            k.get("ws", h.wsp()), k.get("wsb", need), None)
+    assert f(dim=6) == tc.TC_ERR_UNSUPPORTED and "tc_embed_forward_cast" in _err(tc)
+    assert f(dim=2048) == tc.TC_ERR_UNSUPPORTED
+    assert f(W=None) == tc.TC_ERR_INVALID_ARG and "null" in _err(tc)
+    assert f(out=None) == tc.TC_ERR_INVALID_ARG
+    assert f(out=h.fp(misalign=True)) == tc.TC_ERR_UNSUPPORTED
+    assert f(T=-1) == tc.TC_ERR_INVALID_ARG
+    # the cast's own checks, before the forward is launched
+    assert f(wsb=need - 1) == tc.TC_ERR_WORKSPACE
+    assert f(n=2 ** 31) == tc.TC_ERR_INVALID_ARG
+    assert f(rows=2 ** 31) == tc.TC_ERR_INVALID_ARG
+    assert f(cs=None) == tc.TC_ERR_INVALID_ARG
+    assert f(mtr=-1) == tc.TC_ERR_INVALID_ARG
     assert h.untouched()
 
 

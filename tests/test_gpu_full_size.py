@@ -1,7 +1,8 @@
 """All five workloads at full size, one step each, in the launch
-configuration the benchmark times (backward and update fused, with the
-backward workspace, so segments of 2048 pairs or more are summed in pieces;
-the coalesced rows are also stored, to be checked). The casted index is
+configuration the benchmark times (forward and cast as one call, backward
+and update as one, with the backward workspace, so segments of 2048 pairs
+or more are summed in pieces; the coalesced rows are also stored, to be
+checked). The casted index is
 compared with the oracle's in full (bit for bit); forward rows, coalesced
 gradients and updated rows are compared on samples the oracle computes on
 their own: a sampled bag needs only its own pairs, a sampled table row only

@@ -30,12 +30,13 @@ def global_rows(w, b):
 
 
 @pytest.mark.parametrize("bound,fused", [("table-local", True), ("table-local", False),
-                                         ("global", False)])
+                                         ("global", True), ("global", False)])
 @pytest.mark.parametrize("name", list(SMALL))
 def test_two_steps_match_oracle(name, bound, fused):
     """bound: the cast sorts on table-local rows (the table size is passed as
-    the bound) or on global rows (no bound). fused: backward and update as
-    one call (tc_embed_backward_update) or as two."""
+    the bound) or on global rows (no bound). fused: forward and cast as one
+    call (tc_embed_forward_cast) and backward and update as one
+    (tc_embed_backward_update), or all four calls one by one."""
     w = SMALL[name]
     batches = [wl.make_batch(w, s) for s in (0, 1)]
     touched = np.unique(np.concatenate([global_rows(w, b) for b in batches]))
