@@ -218,10 +218,11 @@ def tc_embed_coalesce(expanded, num_pairs, seg_offsets, sorted_pos, num_unique, 
 
 
 class EmbeddingTrainer:
-    """Device buffers for one workload shape and the four calls of a step.
+    """Device buffers for one workload shape and the calls of a step.
 
-    Buffers are torch tensors (device memory only); the step itself is the
-    four library calls on the current stream, with no host synchronisation.
+    Buffers are torch tensors (device memory only); the step itself is
+    library calls on the current stream (forward and cast, then backward and
+    update, each pair one call or two), with no host synchronisation.
     """
 
     def __init__(self, *, total_rows: int, dim: int, num_tables: int, bags_per_table: int,
