@@ -507,35 +507,44 @@ __global__ __launch_bounds__(kLongThreads) void k_backward_long(
 // Long segments with a workspace: persistent blocks take work items
 // (index / parts = list entry: pieces, then long segments of at least
 // kBigLong pairs, then the shorter ones; index % parts = part) from an
-// agent-scope counter until the lists are drained. The next item is fetched
-// while the current one runs.
+// agent-scope counter until the lists are drained. The next item and its
+// list entry are fetched while the current one runs.
 __global__ __launch_bounds__(kLongThreads, 3) void k_backward_list(
     const float *__restrict__ grad, int32_t dim, const int32_t *__restrict__ ids, RowSink sink,
     SplitWs ws) {
     __shared__ LongLds lds;
-    __shared__ int32_t next_item;
+    // the next item and its list entry, in two slots used in turn
+    __shared__ int32_t next_item[2];
+    __shared__ int4 next_entry[2];
     const int lane = threadIdx.x & (kWave - 1);
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int32_t np = min(ws.ctr[0], ws.max_pieces);
     const int32_t nb = min(ws.ctr[1], ws.max_longs);
     const int32_t ns = min(ws.ctr[2], ws.max_longs - nb);
     const int64_t total = int64_t(np + nb + ns) * ws.parts;
-    if (threadIdx.x == 0)
-        next_item = __hip_atomic_fetch_add(&ws.ctr[3], 1, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
+    // thread 0: take the next item and load its list entry into slot s
+    auto take = [&](int s) {
+        const int32_t i = __hip_atomic_fetch_add(&ws.ctr[3], 1, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+        next_item[s] = i;
+        if (i < total) {
+            const int32_t k = i / ws.parts;
+            next_entry[s] = k < np        ? ws.pieces[k]
+                            : k < np + nb ? ws.longs[k - np]
+                                          : ws.longs[ws.max_longs - 1 - (k - np - nb)];
+        }
+    };
+    if (threadIdx.x == 0) take(0);
     lds_barrier();
-    int32_t item = next_item;
+    int slot = 0;
+    int32_t item = next_item[0];
     if (w == 0) __builtin_amdgcn_s_setprio(3);
     while (item < total) {
-        int32_t ahead = 0;
-        if (threadIdx.x == 0)
-            ahead = __hip_atomic_fetch_add(&ws.ctr[3], 1, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
+        const int4 e = next_entry[slot];
+        // the item after this one, visible after this item's last barrier
+        if (threadIdx.x == 0) take(slot ^ 1);
         const int32_t k = item / ws.parts, part = item % ws.parts;
         const int32_t col = part * kPartCols + lane;
-        const int4 e = k < np        ? ws.pieces[k]
-                       : k < np + nb ? ws.longs[k - np]
-                                     : ws.longs[ws.max_longs - 1 - (k - np - nb)];
         const int32_t u = __builtin_amdgcn_readfirstlane(e.x);
         const int32_t beg = __builtin_amdgcn_readfirstlane(e.y);
         const int32_t len = __builtin_amdgcn_readfirstlane(e.z);
@@ -553,9 +562,8 @@ __global__ __launch_bounds__(kLongThreads, 3) void k_backward_list(
             if (w == 0 && col < dim) sink_value(sink, u, dim, col, acc, sv);
         }
         lds_barrier();  // every wavefront is past this item
-        if (threadIdx.x == 0) next_item = ahead;
-        lds_barrier();
-        item = next_item;
+        slot ^= 1;
+        item = next_item[slot];
     }
 }
 
