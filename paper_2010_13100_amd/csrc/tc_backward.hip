@@ -111,7 +111,7 @@ __device__ __forceinline__ int32_t piece_begin(int32_t beg, int32_t len, int32_t
 
 // Buffer resource word 3 for gfx9-family buffers; out-of-range reads give 0.
 constexpr int32_t kBufferWord3 = 0x00020000;
-// A buffer offset past every resource here (resources span < 2^31 bytes):
+// A buffer offset past every resource here (resources span at most this):
 // rows past the end of a segment load as +0.0, which leaves the sum unchanged
 // (a sum started at +0.0 is never -0.0, and x + 0.0 == x for every other x).
 constexpr int32_t kOutOfRange = 0x7ffff000;
@@ -386,20 +386,28 @@ __device__ float long_consumer(LongLds &lds, int32_t nchunks) {
 // The ordered chain over ids[beg, beg + len) for this block's part, run by
 // all five wavefronts (each executes the same number of barriers). Returns
 // the sum of column `col` in the consumer wavefront (w == 0), 0 elsewhere.
+// grad_bytes: the size of the whole grad array when it is at most
+// kOutOfRange (its rows are then addressed from its start), else 0 (the
+// chain's rows are addressed from its first row).
 __device__ __forceinline__ float run_chain(LongLds &lds, const float *__restrict__ grad,
                                            int32_t dim, const int32_t *__restrict__ ids,
                                            int32_t beg, int32_t len, int w, int32_t part,
-                                           int32_t col) {
+                                           int32_t col, int32_t grad_bytes) {
     const int32_t row_bytes = dim * 4;
     const int32_t *sid = ids + beg;
-    // ids within a segment are non-decreasing (stable cast order)
-    const int32_t first = __builtin_amdgcn_readfirstlane(sid[0]);
-    const int32_t last = __builtin_amdgcn_readfirstlane(sid[len - 1]);
-    const uint64_t span = uint64_t(last - first + 1) * uint64_t(row_bytes);
-    if (span >= (uint64_t(1) << 31) || len >= (1 << 29)) {
-        // rows spread over 2 GiB or more (or a segment too long for 32-bit
-        // byte offsets of its ids): the consumer alone, with 64-bit addressed
-        // loads (no barriers on this path)
+    int32_t first = 0;
+    uint64_t span = uint64_t(grad_bytes);
+    if (grad_bytes == 0) {  // uniform
+        // ids within a segment are non-decreasing (stable cast order)
+        first = __builtin_amdgcn_readfirstlane(sid[0]);
+        const int32_t last = __builtin_amdgcn_readfirstlane(sid[len - 1]);
+        span = uint64_t(last - first + 1) * uint64_t(row_bytes);
+    }
+    if (span > uint64_t(kOutOfRange) || len >= (1 << 29)) {
+        // rows spread over about 2 GiB or more, so that kOutOfRange would not
+        // be past them (or a segment too long for 32-bit byte offsets of its
+        // ids): the consumer alone, with 64-bit addressed loads (no barriers
+        // on this path)
         float acc = 0.f;
         if (w == 0) {
             const float *colp = grad + (col < dim ? col : dim - 1);
@@ -459,7 +467,7 @@ __device__ void finish_piece(const SplitWs &ws, const RowSink &sink, int32_t dim
 __global__ __launch_bounds__(kLongThreads) void k_backward_long(
     const float *__restrict__ grad, int32_t dim, const int32_t *__restrict__ ids,
     const int32_t *__restrict__ offsets, const int32_t *__restrict__ num_out_dev,
-    int64_t num_out_cap, RowSink sink) {
+    int64_t num_out_cap, RowSink sink, int32_t grad_bytes) {
     __shared__ LongLds lds;
     const int lane = threadIdx.x & (kWave - 1);
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -497,7 +505,8 @@ __global__ __launch_bounds__(kLongThreads) void k_backward_long(
                 const int64_t seg = c0 + int64_t(kWave) * i + j;
                 SinkVal sv{0, 0.f, 0.f};
                 if (w == 0) sv = sink_value_load(sink, seg, dim, col);
-                const float acc = run_chain(lds, grad, dim, ids, beg, len, w, part, col);
+                const float acc =
+                    run_chain(lds, grad, dim, ids, beg, len, w, part, col, grad_bytes);
                 if (w == 0 && col < dim) sink_value(sink, seg, dim, col, acc, sv);
             }
         }
@@ -511,7 +520,7 @@ __global__ __launch_bounds__(kLongThreads) void k_backward_long(
 // list entry are fetched while the current one runs.
 __global__ __launch_bounds__(kLongThreads, 3) void k_backward_list(
     const float *__restrict__ grad, int32_t dim, const int32_t *__restrict__ ids, RowSink sink,
-    SplitWs ws) {
+    SplitWs ws, int32_t grad_bytes) {
     __shared__ LongLds lds;
     // the next item and its list entry, in two slots used in turn
     __shared__ int32_t next_item[2];
@@ -553,12 +562,13 @@ __global__ __launch_bounds__(kLongThreads, 3) void k_backward_list(
             const int32_t n = num_pieces(len);
             const int32_t p0 = piece_begin(beg, len, n, q);
             const int32_t p1 = piece_begin(beg, len, n, q + 1);
-            const float acc = run_chain(lds, grad, dim, ids, p0, p1 - p0, w, part, col);
+            const float acc =
+                run_chain(lds, grad, dim, ids, p0, p1 - p0, w, part, col, grad_bytes);
             if (w == 0) finish_piece(ws, sink, dim, part, col, u, beg, len, n, q, acc);
         } else {
             SinkVal sv{0, 0.f, 0.f};
             if (w == 0) sv = sink_value_load(sink, u, dim, col);
-            const float acc = run_chain(lds, grad, dim, ids, beg, len, w, part, col);
+            const float acc = run_chain(lds, grad, dim, ids, beg, len, w, part, col, grad_bytes);
             if (w == 0 && col < dim) sink_value(sink, u, dim, col, acc, sv);
         }
         lds_barrier();  // every wavefront is past this item
@@ -760,9 +770,14 @@ int list_blocks() {
     return blocks;
 }
 
-tc_status launch_backward(const float *grad, int32_t dim, const int32_t *ids,
-                          const int32_t *offsets, const int32_t *num_out_dev, int64_t cap,
-                          const RowSink &out, const SplitWs &ws, hipStream_t stream) {
+tc_status launch_backward(const float *grad, int64_t grad_rows, int32_t dim,
+                          const int32_t *ids, const int32_t *offsets,
+                          const int32_t *num_out_dev, int64_t cap, const RowSink &out,
+                          const SplitWs &ws, hipStream_t stream) {
+    // the long chains address rows from the start of grad when it fits in a
+    // 32-bit buffer window with kOutOfRange past its end
+    const int64_t gb = grad_rows * int64_t(dim) * 4;
+    const int32_t grad_bytes = gb <= kOutOfRange ? int32_t(gb) : 0;
     if (ws.cap_pairs > 0) {
         k_backward_init<<<1, kWave, 0, stream>>>(ws);
         const tc_status st = check_launch("k_backward_init");
@@ -797,13 +812,15 @@ tc_status launch_backward(const float *grad, int32_t dim, const int32_t *ids,
     tc_status st = check_launch("k_backward_short");
     if (st != TC_OK) return st;
     if (ws.cap_pairs > 0) {
-        k_backward_list<<<list_blocks(), kLongThreads, 0, stream>>>(grad, dim, ids, out, ws);
+        k_backward_list<<<list_blocks(), kLongThreads, 0, stream>>>(grad, dim, ids, out, ws,
+                                                                     grad_bytes);
         return check_launch("k_backward_list");
     }
     const int parts = (dim + kPartCols - 1) / kPartCols;
     const int ranges = kLongRanges / parts > 64 ? kLongRanges / parts : 64;
     k_backward_long<<<dim3(ranges, parts), kLongThreads, 0, stream>>>(grad, dim, ids, offsets,
-                                                                       num_out_dev, cap, out);
+                                                                       num_out_dev, cap, out,
+                                                                       grad_bytes);
     return check_launch("k_backward_long");
 }
 
@@ -832,8 +849,9 @@ extern "C" tc_status tc_embed_backward(const float *grad_out, int32_t num_bags, 
     TC_REQUIRE(workspace_bytes == 0 || (workspace && aligned16(workspace)), TC_ERR_INVALID_ARG,
                "tc_embed_backward: workspace must be a 16-byte aligned pointer");
     const RowSink sink{coal_grad, nullptr, nullptr, nullptr, TC_OPT_SGD, 0.f, 0.f, 0.f, 1.f};
-    return launch_backward(grad_out, dim, casted_src, seg_offsets, num_unique, max_unique, sink,
-                           make_split_ws(workspace, workspace_bytes, dim), stream);
+    return launch_backward(grad_out, num_bags, dim, casted_src, seg_offsets, num_unique,
+                           max_unique, sink, make_split_ws(workspace, workspace_bytes, dim),
+                           stream);
 }
 
 extern "C" tc_status tc_embed_backward_update(
@@ -870,8 +888,9 @@ extern "C" tc_status tc_embed_backward_update(
                "tc_embed_backward_update: workspace must be a 16-byte aligned pointer");
     const RowSink sink{coal_grad, W, opt_state, unique_rows, opt_kind, lr, eps, gamma,
                        1.0f - gamma};
-    return launch_backward(grad_out, dim, casted_src, seg_offsets, num_unique, max_unique, sink,
-                           make_split_ws(workspace, workspace_bytes, dim), stream);
+    return launch_backward(grad_out, num_bags, dim, casted_src, seg_offsets, num_unique,
+                           max_unique, sink, make_split_ws(workspace, workspace_bytes, dim),
+                           stream);
 }
 
 extern "C" tc_status tc_embed_expand(const float *grad_out, int32_t num_bags, int32_t dim,
@@ -914,8 +933,9 @@ extern "C" tc_status tc_embed_coalesce(const float *expanded, int64_t num_pairs,
     // Algorithm 1's accumulate is the casted gather-reduce over the expanded
     // rows, in sorted order: the same kernels with sorted positions as ids.
     const RowSink sink{coal_grad, nullptr, nullptr, nullptr, TC_OPT_SGD, 0.f, 0.f, 0.f, 1.f};
-    return launch_backward(expanded, dim, sorted_pos, seg_offsets, num_unique, max_unique, sink,
-                           make_split_ws(workspace, workspace_bytes, dim), stream);
+    return launch_backward(expanded, num_pairs, dim, sorted_pos, seg_offsets, num_unique,
+                           max_unique, sink, make_split_ws(workspace, workspace_bytes, dim),
+                           stream);
 }
 
 extern "C" size_t tc_backward_workspace_bytes(int64_t num_pairs, int32_t dim) {
