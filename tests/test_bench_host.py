@@ -41,3 +41,22 @@ def _run(*a):
 def test_more_than_one_gpu_is_refused():
     r = _run("--gpus", "2")
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_step_calls_per_flag():
+    """The calls one timed step makes: forward and cast in one call unless
+    --no-overlap or --unfused, backward and update in one pass unless
+    --unfused or the optimizer is row-wise Adagrad."""
+    import argparse
+    ns = lambda **k: argparse.Namespace(**{"unfused": False, "no_overlap": False, **k})  # noqa
+    c2 = wl.WORKLOADS["c2"]
+    rw = wl.variant(c2, optimizer="rowwise_adagrad")
+    assert bench.step_calls(ns(), c2) == ["forward_cast", "backward_update"]
+    assert bench.step_calls(ns(no_overlap=True), c2) == ["forward", "cast", "backward_update"]
+    assert bench.step_calls(ns(unfused=True), c2) == ["forward", "cast", "backward", "update"]
+    assert bench.step_calls(ns(), rw) == ["forward_cast", "backward", "update"]
+    # every call has its algorithmic bytes, kernels and sources
+    b = bench.algorithmic_bytes(c2, 1000, 300, 40)
+    for c in ("forward_cast", "forward", "cast", "backward_update", "backward", "update"):
+        assert c in b and c in bench.KERNEL_NAMES and c in bench.KERNEL_SOURCES
+    assert b["forward_cast"] == b["forward"] + b["cast"]
