@@ -1,11 +1,15 @@
 // Tensor Casting (Algorithm 2) on CDNA4.
 //
-//  1. k_build_keys   -- (src, dst) pairs from the bag-major CSR index:
-//                       key = row, value = bag id. Block 0 also lays out the
-//                       sort segments (below).
+//  1. k_build_hist   -- (src, dst) pairs from the bag-major CSR index, one
+//                       workgroup per sort tile: key = row, value = bag id
+//                       (each pair's bag found by a search of the bag
+//                       offsets), and the tile's digit counts for the first
+//                       radix pass. Block 0 also writes the tile records of
+//                       the sort segments (below).
 //  2. LSD radix sort by key, stable, at most kMaxRadixBits bits per pass over
 //     the key bits that can be set. Each pass is
-//       k_radix_hist    per-tile digit counts (LDS histograms, one per wave)
+//       k_radix_hist    per-tile digit counts (LDS histograms, one per wave;
+//                       the first pass has them from k_build_hist)
 //       k_radix_scan    per-digit exclusive scan over tiles (one block/digit)
 //       k_radix_scatter stable scatter: a wave finds the lanes holding equal
 //                       digits with ballots, counts them into its running
@@ -28,7 +32,7 @@
 // kTile pairs (its last tile may be short), tiles of all segments are
 // numbered in segment order, and a digit's position inside its segment comes
 // from the per-digit scan over all tiles minus that scan at the segment's
-// first tile. k_build_keys writes one record per tile (its pair range and its
+// first tile. k_build_hist writes one record per tile (its pair range and its
 // segment's), so a pass kernel finds its tile with a single load. Without a
 // bound there is one segment, all pairs on global rows, and tiles are plain
 // slices of kTile pairs.
@@ -37,6 +41,10 @@
 // walks them 64 at a time, lane l taking position base + 64*i + l, so tile
 // order = (wave, iteration, lane) order and every pass is stable. No atomics
 // on global memory; nothing here depends on scheduling order.
+//
+// tc_embed_forward_cast runs the forward gather-reduce in the cast's
+// launches: k_forward_build (k_build_hist's tiles, then workgroups of the
+// forward) or, for a small batch, beside the one k_cast_small workgroup.
 #include "tc_group_sum.h"
 
 namespace tc {
@@ -89,114 +97,196 @@ struct alignas(16) TileRec {
     int32_t p0, p1, first, next, pstart, rowoff, s, pad;
 };
 // ---------------------------------------------------------------------------
-// 1. key build. The tile records of the num_tables segments (table-local
-// sort), written by one whole workgroup.
-__device__ void write_tile_records(const int32_t *__restrict__ bag_offsets,
-                                   const int64_t *__restrict__ table_row_offset,
-                                   int64_t num_bags, int32_t bags_per_table, int32_t num_tables,
-                                   TileRec *__restrict__ tiles, int32_t num_tile_slots) {
-    __shared__ int32_t tstart[kMaxSegTables + 1], pstart[kMaxSegTables + 1];
-    __shared__ int32_t rowoff[kMaxSegTables];
+// 1. key build. The segments of the table-local sort, in LDS: segment s has
+// tiles [tstart[s], tstart[s+1]) and pairs [pstart[s], pstart[s+1]), and
+// rowoff[s] is its table's first row. seg_layout fills it (whole workgroup)
+// and returns the number of tiles; tile_record reads tile b's record off it.
+struct SegLayout {
+    int32_t tstart[kMaxSegTables + 1], pstart[kMaxSegTables + 1], rowoff[kMaxSegTables];
+};
+
+__device__ int32_t seg_layout(SegLayout &L, const int32_t *__restrict__ bag_offsets,
+                              const int64_t *__restrict__ table_row_offset, int64_t num_bags,
+                              int32_t bags_per_table, int32_t num_tables) {
     const int t = threadIdx.x;
     int32_t p0 = 0, n_t = 0;
     if (t < num_tables) {
         p0 = bag_offsets[int64_t(t) * bags_per_table];
         n_t = bag_offsets[int64_t(t + 1) * bags_per_table] - p0;
-        rowoff[t] = int32_t(table_row_offset[t]);
+        L.rowoff[t] = int32_t(table_row_offset[t]);
     }
     int32_t total;
     const int32_t ts = block_exclusive_scan((n_t + kTile - 1) / kTile, &total);
     if (t < num_tables) {
-        tstart[t] = ts;
-        pstart[t] = p0;
+        L.tstart[t] = ts;
+        L.pstart[t] = p0;
     }
     if (t == 0) {
-        tstart[num_tables] = total;
-        pstart[num_tables] = bag_offsets[num_bags];
+        L.tstart[num_tables] = total;
+        L.pstart[num_tables] = bag_offsets[num_bags];
     }
     __syncthreads();
-    for (int32_t b = t; b < num_tile_slots; b += kBlock) {
-        TileRec r{0, 0, 0, 0, 0, 0, -1, 0};
-        if (b < total) {
-            // the segment holding tile b: last s with tstart[s] <= b
-            // (segments without pairs have no tiles and are passed over)
-            int32_t lo = 0, hi = num_tables - 1;
-            while (lo < hi) {
-                const int32_t mid = (lo + hi + 1) / 2;
-                if (tstart[mid] <= b) lo = mid; else hi = mid - 1;
+    return total;
+}
+
+__device__ TileRec tile_record(const SegLayout &L, int32_t num_tables, int32_t total, int32_t b) {
+    TileRec r{0, 0, 0, 0, 0, 0, -1, 0};
+    if (b < total) {
+        // the segment holding tile b: last s with tstart[s] <= b (segments
+        // without pairs have no tiles and are passed over)
+        int32_t lo = 0, hi = num_tables - 1;
+        while (lo < hi) {
+            const int32_t mid = (lo + hi + 1) / 2;
+            if (L.tstart[mid] <= b) lo = mid; else hi = mid - 1;
+        }
+        const int32_t sg = lo;
+        r.s = sg;
+        r.first = L.tstart[sg];
+        r.next = L.tstart[sg + 1];
+        r.pstart = L.pstart[sg];
+        r.rowoff = L.rowoff[sg];
+        r.p0 = L.pstart[sg] + (b - r.first) * kTile;
+        const int32_t end = L.pstart[sg + 1];
+        r.p1 = r.p0 + kTile < end ? r.p0 + kTile : end;
+    }
+    return r;
+}
+
+// Bag offsets staged per tile by build_tile (a 2048-pair tile spans at most
+// 2048 bags with pairs; more only with bags without pairs between them).
+constexpr int kStageBags = 2048;
+
+// One sort tile's (src, dst) pairs, with the tile's digit counts for the
+// first radix pass (digits key & mask0, counts[digit * tiles + b], as
+// k_radix_hist writes them): keys are table-local rows when `local`, else
+// global rows; values are bag ids (dst), or pair positions when `positions`
+// (an argsort). Pair j's bag comes from a search: the bag holding the tile's
+// first pair by a 64-way search of the segment's bag offsets, then each
+// pair's by binary search of the tile's bag offsets staged in LDS. Tile b
+// has its record from the segment layout (local; workgroup 0 also writes
+// every tile's record) or is pairs [b*kTile, (b+1)*kTile) of one segment.
+__device__ void build_tile(int32_t b, const int32_t *__restrict__ indices,
+                           const int32_t *__restrict__ bag_offsets,
+                           const int64_t *__restrict__ table_row_offset, int64_t num_bags,
+                           int32_t bags_per_table, int32_t num_tables, int32_t n, bool local,
+                           bool positions, TileRec *__restrict__ recs, int32_t tiles,
+                           int32_t *__restrict__ keys, int32_t *__restrict__ vals,
+                           int32_t *__restrict__ counts, uint32_t mask0) {
+    __shared__ SegLayout L;
+    __shared__ int32_t sbo[kStageBags + 1];
+    __shared__ int32_t hist[kSortWaves][kMaxRadix];
+    __shared__ int32_t s_g0;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+    TileRec tr{0, 0, 0, 0, 0, 0, -1, 0};
+    int64_t glo = 0, ghi = num_bags;  // the bags of the tile's segment
+    if (local) {
+        const int32_t total = seg_layout(L, bag_offsets, table_row_offset, num_bags,
+                                         bags_per_table, num_tables);
+        if (b == 0)
+            for (int32_t bb = tid; bb < tiles; bb += kBlock)
+                recs[bb] = tile_record(L, num_tables, total, bb);
+        tr = tile_record(L, num_tables, total, b);
+        glo = int64_t(tr.s) * bags_per_table;
+        ghi = glo + bags_per_table;
+    } else if (int64_t(b) * kTile < n) {
+        tr.s = 0;
+        tr.p0 = b * kTile;
+        tr.p1 = tr.p0 + kTile < n ? tr.p0 + kTile : n;
+    }
+    for (int i = tid; i < kSortWaves * kMaxRadix; i += kBlock) (&hist[0][0])[i] = 0;
+    if (tr.s >= 0) {  // uniform
+        const int32_t p0 = tr.p0, p1 = tr.p1;
+        if (w == 0) {
+            // the last bag g in [glo, ghi) with bag_offsets[g] <= p0, the
+            // range narrowed 64-fold per step
+            int64_t lo = glo, hi = ghi;
+            while (hi - lo > 1) {
+                const int64_t step = (hi - lo + kWave - 1) / kWave;
+                const int64_t g = lo + lane * step;
+                const bool le = g < hi && bag_offsets[g] <= p0;
+                const uint64_t m = __ballot(le);
+                const int l = m ? 63 - __builtin_clzll(m) : 0;
+                lo = lo + l * step;
+                hi = lo + step < hi ? lo + step : hi;
             }
-            const int32_t sg = lo;
-            r.s = sg;
-            r.first = tstart[sg];
-            r.next = tstart[sg + 1];
-            r.pstart = pstart[sg];
-            r.rowoff = rowoff[sg];
-            r.p0 = pstart[sg] + (b - r.first) * kTile;
-            const int32_t end = pstart[sg + 1];
-            r.p1 = r.p0 + kTile < end ? r.p0 + kTile : end;
+            if (lane == 0) s_g0 = int32_t(lo);
         }
-        tiles[b] = r;
+        __syncthreads();
+        const int64_t g0 = s_g0;
+        const int32_t nst = int32_t(ghi - g0 < kStageBags ? ghi - g0 : kStageBags);
+        for (int32_t i = tid; i <= nst; i += kBlock) sbo[i] = bag_offsets[g0 + i];
+        __syncthreads();
+        // whether the staged offsets hold the bag of every pair of the tile
+        const bool staged = g0 + nst == ghi || sbo[nst] >= p1;
+#pragma unroll
+        for (int i = 0; i < kItems; ++i) {
+            const int32_t j = p0 + i * kBlock + tid;
+            if (j < p1) {
+                int64_t g;
+                if (staged) {
+                    int32_t lo = 0, hi = nst - 1;
+                    while (lo < hi) {
+                        const int32_t mid = (lo + hi + 1) / 2;
+                        if (sbo[mid] <= j) lo = mid; else hi = mid - 1;
+                    }
+                    g = g0 + lo;
+                } else {
+                    int64_t lo = g0, hi = ghi - 1;
+                    while (lo < hi) {
+                        const int64_t mid = (lo + hi + 1) / 2;
+                        if (bag_offsets[mid] <= j) lo = mid; else hi = mid - 1;
+                    }
+                    g = lo;
+                }
+                const int32_t idx = indices[j];
+                const int32_t key =
+                    local ? idx : int32_t(table_row_offset[g / bags_per_table] + idx);
+                keys[j] = key;
+                vals[j] = positions ? j : int32_t(g);
+                atomicAdd(&hist[w][uint32_t(key) & mask0], 1);
+            }
+        }
+    }
+    __syncthreads();
+    for (uint32_t d = tid; d <= mask0; d += kBlock) {
+        int32_t c = 0;
+#pragma unroll
+        for (int ww = 0; ww < kSortWaves; ++ww) c += hist[ww][d];
+        counts[int64_t(d) * tiles + b] = c;
     }
 }
 
-// (src, dst) pairs: one group of 16 lanes per bag writes that bag's pairs;
-// keys are table-local rows when `local`, else global rows; values are bag
-// ids (dst), or pair positions when `positions` (an argsort). Workgroup
-// `block` of `nblocks` takes every nblocks-th run of bags; with `local`,
-// block 0 also writes the tile records of the num_tables segments.
-__device__ __forceinline__ void build_pairs(
-    int64_t block, int64_t nblocks, const int32_t *__restrict__ indices,
-    const int32_t *__restrict__ bag_offsets, const int64_t *__restrict__ table_row_offset,
-    int64_t num_bags, int32_t bags_per_table, int32_t num_tables, bool local, bool positions,
-    TileRec *__restrict__ tiles, int32_t num_tile_slots, int32_t *__restrict__ keys,
-    int32_t *__restrict__ vals) {
-    if (local && block == 0)
-        write_tile_records(bag_offsets, table_row_offset, num_bags, bags_per_table, num_tables,
-                           tiles, num_tile_slots);
-    constexpr int kLanes = 16;
-    const int64_t group = (block * kBlock + threadIdx.x) / kLanes;
-    const int64_t ngroups = (nblocks * kBlock) / kLanes;
-    const int sub = threadIdx.x & (kLanes - 1);
-    for (int64_t g = group; g < num_bags; g += ngroups) {
-        const int32_t beg = bag_offsets[g], end = bag_offsets[g + 1];
-        const int64_t base = local ? 0 : table_row_offset[g / bags_per_table];
-        for (int32_t j = beg + sub; j < end; j += kLanes) {
-            keys[j] = int32_t(base + indices[j]);
-            vals[j] = positions ? j : int32_t(g);
-        }
-    }
-}
-
-__global__ __launch_bounds__(kBlock) void k_build_keys(
+// The pairs and first-pass digit counts of every sort tile (tc_cast_index,
+// tc_argsort_rows): one workgroup per tile slot.
+__global__ __launch_bounds__(kBlock) void k_build_hist(
     const int32_t *__restrict__ indices, const int32_t *__restrict__ bag_offsets,
     const int64_t *__restrict__ table_row_offset, int64_t num_bags, int32_t bags_per_table,
-    int32_t num_tables, bool local, bool positions, TileRec *__restrict__ tiles,
-    int32_t num_tile_slots, int32_t *__restrict__ keys, int32_t *__restrict__ vals) {
-    build_pairs(blockIdx.x, gridDim.x, indices, bag_offsets, table_row_offset, num_bags,
-                bags_per_table, num_tables, local, positions, tiles, num_tile_slots, keys, vals);
+    int32_t num_tables, int32_t n, bool local, bool positions, TileRec *__restrict__ recs,
+    int32_t tiles, int32_t *__restrict__ keys, int32_t *__restrict__ vals,
+    int32_t *__restrict__ counts, uint32_t mask0) {
+    build_tile(blockIdx.x, indices, bag_offsets, table_row_offset, num_bags, bags_per_table,
+               num_tables, n, local, positions, recs, tiles, keys, vals, counts, mask0);
 }
 
-// The key build and the forward gather-reduce in one launch
-// (tc_embed_forward_cast): the first build_blocks workgroups build the pairs
-// as k_build_keys does, the others run the forward (FL lanes per bag, as
-// k_forward). Both read the index array; kept in separate workgroups, the
-// pair stores stay out of the forward's chains of dependent loads.
+// The same with the forward gather-reduce in one launch
+// (tc_embed_forward_cast): the first `tiles` workgroups build one sort tile
+// each, the others run the forward (FL lanes per bag, as k_forward). Both
+// read the index array; the tile workgroups' searches and stores stay out of
+// the forward's chains of dependent loads, and their latency hides behind
+// the forward's.
 template <int FL>
-__global__ __launch_bounds__(kBlock) void k_forward_keys(FwdSlice f, int32_t build_blocks,
-                                                         int32_t num_tables, bool local,
-                                                         TileRec *__restrict__ tiles,
-                                                         int32_t num_tile_slots,
-                                                         int32_t *__restrict__ keys,
-                                                         int32_t *__restrict__ vals) {
-    if (int32_t(blockIdx.x) < build_blocks) {  // uniform
-        build_pairs(blockIdx.x, build_blocks, f.ids, f.offsets, f.table_row_offset, f.bag_hi,
-                    f.bags_per_table, num_tables, local, false, tiles, num_tile_slots, keys,
-                    vals);
+__global__ __launch_bounds__(kBlock) void k_forward_build(
+    FwdSlice f, int32_t num_tables, int32_t n, bool local, TileRec *__restrict__ recs,
+    int32_t tiles, int32_t *__restrict__ keys, int32_t *__restrict__ vals,
+    int32_t *__restrict__ counts, uint32_t mask0) {
+    if (int32_t(blockIdx.x) < tiles) {  // uniform
+        build_tile(blockIdx.x, f.ids, f.offsets, f.table_row_offset, f.bag_hi, f.bags_per_table,
+                   num_tables, n, local, false, recs, tiles, keys, vals, counts, mask0);
         return;
     }
     constexpr int64_t kWaves = kBlock / kWave;
-    forward_bags<FL, 1>(f, (int64_t(blockIdx.x) - build_blocks) * kWaves + threadIdx.x / kWave,
-                        (int64_t(gridDim.x) - build_blocks) * kWaves);
+    forward_bags<FL, 1>(f, (int64_t(blockIdx.x) - tiles) * kWaves + threadIdx.x / kWave,
+                        (int64_t(gridDim.x) - tiles) * kWaves);
 }
 
 // This block's tile: its record (table-local sort) or a plain slice of the
@@ -739,14 +829,18 @@ __global__ void k_cast_empty(int32_t *seg_offsets, int32_t *num_unique) {
 }
 
 // One LSD pass over `bits` (1..kMaxRadixBits) digit bits starting at `shift`.
+// One radix pass; hist_done: the digit counts are already in `counts` (the
+// first pass, counted by the pair build).
 tc_status launch_radix_pass(int bits, const int32_t *kin, const int32_t *vin, int32_t *kout,
                             int32_t *vout, int32_t n, int shift, const TileRec *recs,
                             int32_t *counts, int32_t *totals, int32_t tiles, bool last,
-                            hipStream_t stream) {
+                            bool hist_done, hipStream_t stream) {
 #define TC_PASS_CASE(B)                                                                      \
     case B:                                                                                  \
-        k_radix_hist<B><<<tiles, kBlock, 0, stream>>>(kin, n, shift, recs, counts, tiles);   \
-        if (check_launch("k_radix_hist") != TC_OK) return TC_ERR_HIP;                        \
+        if (!hist_done) {                                                                    \
+            k_radix_hist<B><<<tiles, kBlock, 0, stream>>>(kin, n, shift, recs, counts, tiles); \
+            if (check_launch("k_radix_hist") != TC_OK) return TC_ERR_HIP;                    \
+        }                                                                                    \
         k_radix_scan<<<1 << B, kBlock, 0, stream>>>(counts, tiles, totals);                  \
         if (check_launch("k_radix_scan") != TC_OK) return TC_ERR_HIP;                        \
         k_radix_scatter<B><<<tiles, kBlock, 0, stream>>>(kin, vin, kout, vout, n, shift,     \
@@ -917,31 +1011,31 @@ tc_status cast_impl(const char *what, bool positions, const int64_t *table_row_o
     const int32_t sort_tiles = int32_t(plan.sort_tiles);
     const int32_t seg_tiles = int32_t(plan.seg_tiles);
 
-    if (fl) {
-        // the key build's workgroups, then the forward's, in one launch
-        const unsigned bb = grid_for(num_bags, kBlock / 16, int64_t(kNumCUs) * 8);
-        const int64_t per_block = int64_t(kBlock / kWave) * (kWave / fl);
-        const unsigned grid = bb + grid_for(num_bags, per_block, int64_t(kNumCUs) * 32);
-#define TC_FWD_KEYS(FL)                                                                      \
-    k_forward_keys<FL><<<grid, kBlock, 0, stream>>>(*fwd, int32_t(bb), num_tables, local,      \
-                                                    recs, sort_tiles, ka, va)
-        if (fl == 16) TC_FWD_KEYS(16);
-        else if (fl == 32) TC_FWD_KEYS(32);
-        else TC_FWD_KEYS(64);
-#undef TC_FWD_KEYS
-        tc_status st = check_launch("k_forward_keys");
-        if (st != TC_OK) return st;
-    } else {
-        const unsigned grid = grid_for(num_bags, kBlock / 16, int64_t(kNumCUs) * 8);
-        k_build_keys<<<grid, kBlock, 0, stream>>>(indices, bag_offsets, table_row_offset,
-                                                  num_bags, bags_per_table, num_tables, local,
-                                                  positions, recs, sort_tiles, ka, va);
-        tc_status st = check_launch("k_build_keys");
-        if (st != TC_OK) return st;
-    }
-
     const int passes = (bits + kMaxRadixBits - 1) / kMaxRadixBits;
     const int per_pass = (bits + passes - 1) / passes;
+    const uint32_t mask0 = (1u << per_pass) - 1u;  // the first pass's digits
+    if (fl) {
+        // the tiles' pair builds, then the forward's workgroups, in one launch
+        const int64_t per_block = int64_t(kBlock / kWave) * (kWave / fl);
+        const unsigned grid =
+            unsigned(sort_tiles) + grid_for(num_bags, per_block, int64_t(kNumCUs) * 32);
+#define TC_FWD_BUILD(FL)                                                                     \
+    k_forward_build<FL><<<grid, kBlock, 0, stream>>>(*fwd, num_tables, int32_t(num_pairs),    \
+                                                     local, recs, sort_tiles, ka, va, counts,  \
+                                                     mask0)
+        if (fl == 16) TC_FWD_BUILD(16);
+        else if (fl == 32) TC_FWD_BUILD(32);
+        else TC_FWD_BUILD(64);
+#undef TC_FWD_BUILD
+        tc_status st = check_launch("k_forward_build");
+        if (st != TC_OK) return st;
+    } else {
+        k_build_hist<<<sort_tiles, kBlock, 0, stream>>>(
+            indices, bag_offsets, table_row_offset, num_bags, bags_per_table, num_tables,
+            int32_t(num_pairs), local, positions, recs, sort_tiles, ka, va, counts, mask0);
+        tc_status st = check_launch("k_build_hist");
+        if (st != TC_OK) return st;
+    }
     int32_t *kin = ka, *vin = va, *kout = kb, *vout = vb;
     for (int p = 0; p < passes; ++p) {
         const int shift = p * per_pass;
@@ -949,7 +1043,7 @@ tc_status cast_impl(const char *what, bool positions, const int64_t *table_row_o
         const bool last = p == passes - 1;
         int32_t *vdst = last ? casted_src : vout;
         tc_status st = launch_radix_pass(pb, kin, vin, kout, vdst, int32_t(num_pairs), shift,
-                                         recs, counts, totals, sort_tiles, last, stream);
+                                         recs, counts, totals, sort_tiles, last, p == 0, stream);
         if (st != TC_OK) return st;
         // next pass reads what this one wrote
         int32_t *tk = kin, *tv = vin;
