@@ -123,3 +123,36 @@ def test_single_workgroup_cast_boundary():
     # the multi-kernel sort
     for n in (8191, 8192, 8193):
         check(f"n={n}", [3000, 500], [n - 600, 600], bags_per_table=9, seed=n)
+
+
+def sparse_bags_case(num_tables, bags_per_table, pairs_per_table, rows, seed):
+    """Bags mostly without pairs: each table's pairs sit in every 4th bag,
+    so a 2048-pair sort tile spans about 8192 bags (more than the pair build
+    stages per tile)."""
+    rng = np.random.default_rng(seed)
+    off = np.arange(num_tables + 1, dtype=np.int64) * rows
+    lengths = np.zeros(num_tables * bags_per_table, np.int64)
+    for t in range(num_tables):
+        full = np.arange(t * bags_per_table, (t + 1) * bags_per_table, 4)
+        per = np.full(len(full), pairs_per_table // len(full))
+        per[: pairs_per_table - per.sum()] += 1
+        lengths[full] = per
+    bo = np.zeros(len(lengths) + 1, np.int64)
+    np.cumsum(lengths, out=bo[1:])
+    idx = rng.integers(0, rows, size=int(bo[-1])).astype(np.int32)
+    return off, bo.astype(np.int32), idx
+
+
+def test_tiles_spanning_many_empty_bags():
+    for bound_name, T, B, P in (("table-local", 2, 40_000, 9_000), ("global", 3, 30_000, 7_000)):
+        off, bo, indices = sparse_bags_case(T, B, P, 5000, seed=T)
+        print(f"\n[sparse bags {bound_name}] tables {T} bags {T * B} pairs {len(indices)}",
+              flush=True)
+        ref = oracle_cast(off, bo, indices, B)
+        n = len(indices)
+        got = gpu_cast(off, bo, indices, B, 5000 if bound_name == "table-local" else 0)
+        assert got["num_unique"] == ref["num_unique"]
+        assert np.array_equal(got["unique_rows"], ref["unique_rows"])
+        assert np.array_equal(got["seg_offsets"], ref["seg_offsets"])
+        assert np.array_equal(got["casted_src"], ref["casted_src"][:n])
+        assert np.array_equal(got["casted_dst"], ref["casted_dst"][:n])

@@ -11,13 +11,14 @@ import torch
 
 import oracle
 from paper_2010_13100_amd import tc
-from tests.test_gpu_cast_layouts import make_case
+from tests.test_gpu_cast_layouts import make_case, sparse_bags_case
 
 pytestmark = pytest.mark.gpu
 
 
-def run_case(name, table_rows, pairs_per_table, bags_per_table, dim, seed, bound=None):
-    off, bo, indices = make_case(table_rows, pairs_per_table, bags_per_table, seed)
+def run_case(name, table_rows, pairs_per_table, bags_per_table, dim, seed, bound=None,
+             case=None):
+    off, bo, indices = case or make_case(table_rows, pairs_per_table, bags_per_table, seed)
     T, n, R = len(table_rows), len(indices), int(off[-1])
     bound = max(table_rows) if bound is None else bound
     print(f"\n[{name} dim={dim} bound={bound}] tables {T} pairs {n}", flush=True)
@@ -90,3 +91,11 @@ def test_no_pairs():
     # every bag empty: rows of zeros and an empty casted index
     run_case("no pairs", [10, 20], [0, 0], 4, 64, seed=6)
     run_case("no pairs, narrow rows", [10, 20], [0, 0], 4, 8, seed=7)
+
+
+def test_tiles_spanning_many_empty_bags():
+    # pairs in every 4th bag: a sort tile spans more bags than are staged
+    case = sparse_bags_case(2, 40_000, 9_000, 5000, seed=8)
+    run_case("sparse bags", [5000, 5000], None, 40_000, 64, seed=8, case=case)
+    case = sparse_bags_case(3, 30_000, 7_000, 5000, seed=9)
+    run_case("sparse bags, global", [5000] * 3, None, 30_000, 128, seed=9, bound=0, case=case)
