@@ -58,7 +58,7 @@ KERNEL_NAMES = {
     "backward": ["k_backward_init", "k_backward_short", "k_backward_list"],
     "backward_update": ["k_backward_init", "k_backward_short", "k_backward_list"],
     "update": ["k_sparse_update"],
-    "cast": ["k_cast_small", "k_build_hist", "k_radix_hist", "k_radix_scan", "k_radix_scatter",
+    "cast": ["k_cast_small", "k_build_keys", "k_radix_hist", "k_radix_scan", "k_radix_scatter",
              "k_seg_count", "k_seg_write"],
     # the forward's bags run inside the scatters (or beside k_cast_small)
     "forward_cast": ["k_cast_small", "k_forward_build", "k_radix_hist", "k_radix_scan",

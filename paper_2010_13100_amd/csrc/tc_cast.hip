@@ -1,15 +1,11 @@
 // Tensor Casting (Algorithm 2) on CDNA4.
 //
-//  1. k_build_hist   -- (src, dst) pairs from the bag-major CSR index, one
-//                       workgroup per sort tile: key = row, value = bag id
-//                       (each pair's bag found by a search of the bag
-//                       offsets), and the tile's digit counts for the first
-//                       radix pass. Block 0 also writes the tile records of
-//                       the sort segments (below).
+//  1. k_build_keys   -- (src, dst) pairs from the bag-major CSR index:
+//                       key = row, value = bag id. Block 0 also writes the
+//                       tile records of the sort segments (below).
 //  2. LSD radix sort by key, stable, at most kMaxRadixBits bits per pass over
 //     the key bits that can be set. Each pass is
-//       k_radix_hist    per-tile digit counts (LDS histograms, one per wave;
-//                       the first pass has them from k_build_hist)
+//       k_radix_hist    per-tile digit counts (LDS histograms, one per wave)
 //       k_radix_scan    per-digit exclusive scan over tiles (one block/digit)
 //       k_radix_scatter stable scatter: a wave finds the lanes holding equal
 //                       digits with ballots, counts them into its running
@@ -32,7 +28,7 @@
 // kTile pairs (its last tile may be short), tiles of all segments are
 // numbered in segment order, and a digit's position inside its segment comes
 // from the per-digit scan over all tiles minus that scan at the segment's
-// first tile. k_build_hist writes one record per tile (its pair range and its
+// first tile. k_build_keys writes one record per tile (its pair range and its
 // segment's), so a pass kernel finds its tile with a single load. Without a
 // bound there is one segment, all pairs on global rows, and tiles are plain
 // slices of kTile pairs.
@@ -43,8 +39,10 @@
 // on global memory; nothing here depends on scheduling order.
 //
 // tc_embed_forward_cast runs the forward gather-reduce in the cast's
-// launches: k_forward_build (k_build_hist's tiles, then workgroups of the
-// forward) or, for a small batch, beside the one k_cast_small workgroup.
+// launches: k_forward_build (pairs and first-pass digit counts built per
+// tile, then workgroups of the forward; the first pass needs no
+// k_radix_hist) or, for a small batch, beside the one k_cast_small
+// workgroup.
 #include "tc_group_sum.h"
 
 namespace tc {
@@ -256,21 +254,49 @@ __device__ void build_tile(int32_t b, const int32_t *__restrict__ indices,
     }
 }
 
-// The pairs and first-pass digit counts of every sort tile (tc_cast_index,
-// tc_argsort_rows): one workgroup per tile slot.
-__global__ __launch_bounds__(kBlock) void k_build_hist(
-    const int32_t *__restrict__ indices, const int32_t *__restrict__ bag_offsets,
-    const int64_t *__restrict__ table_row_offset, int64_t num_bags, int32_t bags_per_table,
-    int32_t num_tables, int32_t n, bool local, bool positions, TileRec *__restrict__ recs,
-    int32_t tiles, int32_t *__restrict__ keys, int32_t *__restrict__ vals,
-    int32_t *__restrict__ counts, uint32_t mask0) {
-    build_tile(blockIdx.x, indices, bag_offsets, table_row_offset, num_bags, bags_per_table,
-               num_tables, n, local, positions, recs, tiles, keys, vals, counts, mask0);
+// The records of all num_tile_slots tile slots, written by one workgroup.
+__device__ void write_tile_records(const int32_t *__restrict__ bag_offsets,
+                                   const int64_t *__restrict__ table_row_offset,
+                                   int64_t num_bags, int32_t bags_per_table, int32_t num_tables,
+                                   TileRec *__restrict__ tiles, int32_t num_tile_slots) {
+    __shared__ SegLayout L;
+    const int32_t total = seg_layout(L, bag_offsets, table_row_offset, num_bags, bags_per_table,
+                                     num_tables);
+    for (int32_t b = threadIdx.x; b < num_tile_slots; b += kBlock)
+        tiles[b] = tile_record(L, num_tables, total, b);
 }
 
-// The same with the forward gather-reduce in one launch
-// (tc_embed_forward_cast): the first `tiles` workgroups build one sort tile
-// each, the others run the forward (FL lanes per bag, as k_forward). Both
+// (src, dst) pairs by a walk over the bags (tc_cast_index, tc_argsort_rows):
+// one group of 16 lanes per bag writes that bag's pairs; keys and values as
+// in build_tile. With `local`, block 0 also writes the tile records. The
+// first pass then counts its digits with k_radix_hist: on its own, this walk
+// and that count take less time than build_tile's searches.
+__global__ __launch_bounds__(kBlock) void k_build_keys(
+    const int32_t *__restrict__ indices, const int32_t *__restrict__ bag_offsets,
+    const int64_t *__restrict__ table_row_offset, int64_t num_bags, int32_t bags_per_table,
+    int32_t num_tables, bool local, bool positions, TileRec *__restrict__ tiles,
+    int32_t num_tile_slots, int32_t *__restrict__ keys, int32_t *__restrict__ vals) {
+    if (local && blockIdx.x == 0)
+        write_tile_records(bag_offsets, table_row_offset, num_bags, bags_per_table, num_tables,
+                           tiles, num_tile_slots);
+    constexpr int kLanes = 16;
+    const int64_t group = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / kLanes;
+    const int64_t ngroups = (int64_t(gridDim.x) * blockDim.x) / kLanes;
+    const int sub = threadIdx.x & (kLanes - 1);
+    for (int64_t g = group; g < num_bags; g += ngroups) {
+        const int32_t beg = bag_offsets[g], end = bag_offsets[g + 1];
+        const int64_t base = local ? 0 : table_row_offset[g / bags_per_table];
+        for (int32_t j = beg + sub; j < end; j += kLanes) {
+            keys[j] = int32_t(base + indices[j]);
+            vals[j] = positions ? j : int32_t(g);
+        }
+    }
+}
+
+// The pair build and the first pass's digit counts (build_tile, one sort
+// tile per workgroup) with the forward gather-reduce in one launch
+// (tc_embed_forward_cast): the first `tiles` workgroups build the tiles,
+// the others run the forward (FL lanes per bag, as k_forward). Both
 // read the index array; the tile workgroups' searches and stores stay out of
 // the forward's chains of dependent loads, and their latency hides behind
 // the forward's.
@@ -1030,10 +1056,11 @@ tc_status cast_impl(const char *what, bool positions, const int64_t *table_row_o
         tc_status st = check_launch("k_forward_build");
         if (st != TC_OK) return st;
     } else {
-        k_build_hist<<<sort_tiles, kBlock, 0, stream>>>(
-            indices, bag_offsets, table_row_offset, num_bags, bags_per_table, num_tables,
-            int32_t(num_pairs), local, positions, recs, sort_tiles, ka, va, counts, mask0);
-        tc_status st = check_launch("k_build_hist");
+        const unsigned grid = grid_for(num_bags, kBlock / 16, int64_t(kNumCUs) * 8);
+        k_build_keys<<<grid, kBlock, 0, stream>>>(indices, bag_offsets, table_row_offset,
+                                                  num_bags, bags_per_table, num_tables, local,
+                                                  positions, recs, sort_tiles, ka, va);
+        tc_status st = check_launch("k_build_keys");
         if (st != TC_OK) return st;
     }
     int32_t *kin = ka, *vin = va, *kout = kb, *vout = vb;
@@ -1043,7 +1070,8 @@ tc_status cast_impl(const char *what, bool positions, const int64_t *table_row_o
         const bool last = p == passes - 1;
         int32_t *vdst = last ? casted_src : vout;
         tc_status st = launch_radix_pass(pb, kin, vin, kout, vdst, int32_t(num_pairs), shift,
-                                         recs, counts, totals, sort_tiles, last, p == 0, stream);
+                                         recs, counts, totals, sort_tiles, last,
+                                         p == 0 && fl != 0, stream);
         if (st != TC_OK) return st;
         // next pass reads what this one wrote
         int32_t *tk = kin, *tv = vin;
