@@ -22,12 +22,15 @@ from tests.gpu_harness import (SPLIT_PAIRS, GpuRun, assert_close, compare_cast, 
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("cfg,split", [("c1", True), ("c2", True), ("c3", True), ("c4", True),
-                                       ("c5", True), ("c2", False), ("c3", False)])
-def test_full_size_step(cfg, split):
+@pytest.mark.parametrize("cfg,split,opt", [("c1", True, None), ("c2", True, None),
+                                           ("c3", True, None), ("c4", True, None),
+                                           ("c5", True, None), ("c2", False, None),
+                                           ("c3", False, None), ("c3", True, "rmsprop")])
+def test_full_size_step(cfg, split, opt):
     """split: with the backward workspace (as the benchmark runs), or without
-    it (every segment one ordered chain, the hottest rows included)."""
-    w = wl.WORKLOADS[cfg]
+    it (every segment one ordered chain, the hottest rows included). opt:
+    another optimizer than the workload's (the same batch and table)."""
+    w = wl.variant(wl.WORKLOADS[cfg], optimizer=opt)
     b = wl.make_batch(w, step=0)
     print(f"\n[{cfg} split={split}] {w.name}: {b.num_pairs} pairs", flush=True)
     run = GpuRun(w, max_pairs=b.num_pairs, split_long=split)
