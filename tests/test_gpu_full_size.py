@@ -2,7 +2,8 @@
 configuration the benchmark times (forward and cast as one call, backward
 and update as one, with the backward workspace, so segments of 2048 pairs
 or more are summed in pieces; the coalesced rows are also stored, to be
-checked). The casted index is
+checked, except in the cases that pass exactly the benchmark's arguments).
+The casted index is
 compared with the oracle's in full (bit for bit); forward rows, coalesced
 gradients and updated rows are compared on samples the oracle computes on
 their own: a sampled bag needs only its own pairs, a sampled table row only
@@ -22,20 +23,24 @@ from tests.gpu_harness import (SPLIT_PAIRS, GpuRun, assert_close, compare_cast, 
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("cfg,split,opt", [("c1", True, None), ("c2", True, None),
-                                           ("c3", True, None), ("c4", True, None),
-                                           ("c5", True, None), ("c2", False, None),
-                                           ("c3", False, None), ("c3", True, "rmsprop")])
-def test_full_size_step(cfg, split, opt):
+@pytest.mark.parametrize("cfg,split,opt,stored", [
+    ("c1", True, None, True), ("c2", True, None, True), ("c3", True, None, True),
+    ("c4", True, None, True), ("c5", True, None, True), ("c2", False, None, True),
+    ("c3", False, None, True), ("c3", True, "rmsprop", True), ("c2", True, None, False),
+    ("c5", True, None, False)])
+def test_full_size_step(cfg, split, opt, stored):
     """split: with the backward workspace (as the benchmark runs), or without
     it (every segment one ordered chain, the hottest rows included). opt:
-    another optimizer than the workload's (the same batch and table)."""
+    another optimizer than the workload's (the same batch and table).
+    stored: casted_dst and the coalesced rows written too; without them the
+    calls take exactly the benchmark's arguments, and the coalesced rows are
+    checked through the updated table rows only."""
     w = wl.variant(wl.WORKLOADS[cfg], optimizer=opt)
     b = wl.make_batch(w, step=0)
-    print(f"\n[{cfg} split={split}] {w.name}: {b.num_pairs} pairs", flush=True)
+    print(f"\n[{cfg} split={split} stored={stored}] {w.name}: {b.num_pairs} pairs", flush=True)
     run = GpuRun(w, max_pairs=b.num_pairs, split_long=split)
     assert run.split_cap >= b.num_pairs if split else run.split_cap == 0
-    run.run_step(b, with_casted_dst=True, fused=True, store_coal=True)
+    run.run_step(b, with_casted_dst=stored, fused=True, store_coal=stored)
     t = run.trainer
     orc = oracle.Oracle("f32")
     src, dst = orc.pairs_from_csr(w.num_tables, w.batch, b.table_row_offset, b.indices,
@@ -72,10 +77,12 @@ def test_full_size_step(cfg, split, opt):
     pieces = np.flatnonzero(seg[pick] >= SPLIT_PAIRS) if run.split_cap else np.zeros(0, int)
     for k in pieces:   # the row's bags in input order = its segment in sorted order
         ref_coal[k] = piecewise_row(orc, dst[src == rows[k]], b.grad_out)
-    got_coal = t.coal.index_select(0, torch.from_numpy(pick).cuda()).cpu().numpy()
-    assert_close(got_coal, ref_coal, f"{cfg} coalesced gradient (sampled rows)", bitwise=True)
-    if len(pieces):
-        assert_close(got_coal[pieces], seq64[pieces], f"{cfg} split rows vs fp64 sums")
+    if stored:
+        got_coal = t.coal.index_select(0, torch.from_numpy(pick).cuda()).cpu().numpy()
+        assert_close(got_coal, ref_coal, f"{cfg} coalesced gradient (sampled rows)",
+                     bitwise=True)
+        if len(pieces):
+            assert_close(got_coal[pieces], seq64[pieces], f"{cfg} split rows vs fp64 sums")
     tbl = wl.table_rows(w, rows)
     acc = None if w.optimizer == "sgd" else np.zeros_like(tbl)
     scatter(orc, w, rows, ref_coal, tbl, acc, rows)
