@@ -531,6 +531,7 @@ __global__ __launch_bounds__(kLongThreads, 3) void k_backward_list(
     const int32_t nb = min(ws.ctr[1], ws.max_longs);
     const int32_t ns = min(ws.ctr[2], ws.max_longs - nb);
     const int64_t total = int64_t(np + nb + ns) * ws.parts;
+    if (total == 0) return;  // uniform: nothing listed (no segment is long)
     // thread 0: take the next item and load its list entry into slot s
     auto take = [&](int s) {
         const int32_t i = __hip_atomic_fetch_add(&ws.ctr[3], 1, __ATOMIC_RELAXED,

@@ -672,6 +672,7 @@ constexpr int kSmallWaves = kSmallThreads / kWave;  // 16
 constexpr int kSmallItems = 8;
 constexpr int kSmallSpan = kWave * kSmallItems;     // 512
 constexpr int kSmallPairs = kSmallWaves * kSmallSpan;  // 8192
+static_assert(kSmallPairs == kSmallItems * kSmallThreads, "k_cast_small stages one item per trip");
 
 // Block-wide exclusive scan over the kSmallThreads threads.
 __device__ __forceinline__ int32_t small_block_scan(int32_t v, int32_t *total) {
@@ -731,10 +732,24 @@ __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
         const bool staged = num_bags < kSmallPairs && num_tables <= kSmallWaves * kMaxRadix;
         int32_t *s_idx = keys[1], *s_bo = vals[1], *s_off = &wcount[0][0];
         if (staged) {
-            for (int32_t j = tid; j < n; j += kSmallThreads) s_idx[j] = indices[j];
-            for (int32_t g = tid; g <= num_bags; g += kSmallThreads) s_bo[g] = bag_offsets[g];
+            // every load issued before the first LDS store (n and num_bags
+            // + 1 are at most kSmallPairs = kSmallItems * kSmallThreads), so
+            // the staging waits for memory once, not once per trip
+            int32_t vi[kSmallItems], vb[kSmallItems];
+#pragma unroll
+            for (int i = 0; i < kSmallItems; ++i) {
+                const int32_t j = tid + i * kSmallThreads;
+                vi[i] = j < n ? indices[j] : 0;
+                vb[i] = j <= num_bags ? bag_offsets[j] : 0;
+            }
             for (int32_t t = tid; t < num_tables; t += kSmallThreads)
                 s_off[t] = int32_t(table_row_offset[t]);
+#pragma unroll
+            for (int i = 0; i < kSmallItems; ++i) {
+                const int32_t j = tid + i * kSmallThreads;
+                if (j < n) s_idx[j] = vi[i];
+                if (j <= num_bags) s_bo[j] = vb[i];
+            }
             __syncthreads();
         }
         for (int32_t g = tid / kLanes; g < num_bags; g += kSmallThreads / kLanes) {
