@@ -663,8 +663,9 @@ __global__ __launch_bounds__(kBlock) void k_seg_write(
 // ---------------------------------------------------------------------------
 // Small batches (at most kSmallPairs pairs): the whole cast in one workgroup
 // of kSmallThreads threads, keys and values in LDS. Same stable LSD passes
-// (wave w owns positions [w*kSmallSpan, (w+1)*kSmallSpan), walked 64 at a
-// time; equal digits ranked with ballots and one LDS atomic per digit group)
+// (the pairs are spread evenly over the wavefronts in whole trips of 64:
+// wave w owns positions [w*span, (w+1)*span), walked 64 at a time; equal
+// digits ranked with ballots and one LDS atomic per digit group)
 // and the same segment build, without the kernel chain: for a few thousand
 // pairs the multi-kernel cast is all launch and memory latency.
 constexpr int kSmallThreads = 1024;
@@ -767,7 +768,10 @@ __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
 
     const int passes = (bits + kMaxRadixBits - 1) / kMaxRadixBits;
     const int per_pass = (bits + passes - 1) / passes;
-    const int32_t base = w * kSmallSpan;
+    // trips of 64 positions per wavefront (at most kSmallItems), so that
+    // every wavefront holds a share of the pairs
+    const int trips = (n + kSmallThreads - 1) / kSmallThreads;
+    const int32_t base = w * trips * kWave;
     int cur = 0;
     for (int p = 0; p < passes; ++p) {
         const int shift = p * per_pass;
@@ -780,6 +784,10 @@ __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
             old[kSmallItems];
 #pragma unroll
         for (int i = 0; i < kSmallItems; ++i) {
+            old[i] = lower_n[i] = 0;
+            leader[i] = lane;
+            key[i] = val[i] = 0;
+            if (i >= trips) continue;  // uniform
             const int32_t j = base + i * kWave + lane;
             const bool ok = j < n;
             key[i] = ok ? keys[cur][j] : 0;
@@ -797,7 +805,7 @@ __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
         int32_t rank[kSmallItems];
 #pragma unroll
         for (int i = 0; i < kSmallItems; ++i)
-            rank[i] = __shfl(old[i], leader[i], kWave) + lower_n[i];
+            rank[i] = i < trips ? __shfl(old[i], leader[i], kWave) + lower_n[i] : 0;
         __syncthreads();
         {
             // digit d = tid (threads past the radix hold zeros): start of each
@@ -821,7 +829,7 @@ __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
         __syncthreads();
 #pragma unroll
         for (int i = 0; i < kSmallItems; ++i) {
-            if (base + i * kWave + lane < n) {
+            if (i < trips && base + i * kWave + lane < n) {
                 const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
                 const int32_t lp = wcount[w][d] + rank[i];
                 keys[cur ^ 1][lp] = key[i];
@@ -832,20 +840,21 @@ __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
         cur ^= 1;
     }
 
-    // segment build: thread tid owns sorted positions tid*8 .. tid*8+7
+    // segment build: thread tid owns sorted positions tid*trips .. tid*trips +
+    // trips - 1
     int32_t head[kSmallItems], c = 0;
 #pragma unroll
     for (int i = 0; i < kSmallItems; ++i) {
-        const int32_t j = tid * kSmallItems + i;
-        head[i] = j < n && (j == 0 || keys[cur][j] != keys[cur][j - 1]);
+        const int32_t j = tid * trips + i;
+        head[i] = i < trips && j < n && (j == 0 || keys[cur][j] != keys[cur][j - 1]);
         c += head[i];
     }
     int32_t total;
     int32_t run = small_block_scan(c, &total);
 #pragma unroll
     for (int i = 0; i < kSmallItems; ++i) {
-        const int32_t j = tid * kSmallItems + i;
-        if (j < n) {
+        const int32_t j = tid * trips + i;
+        if (i < trips && j < n) {
             run += head[i];
             casted_src[j] = vals[cur][j];
             if (casted_dst) casted_dst[j] = run - 1;

@@ -125,6 +125,15 @@ def test_single_workgroup_cast_boundary():
         check(f"n={n}", [3000, 500], [n - 600, 600], bags_per_table=9, seed=n)
 
 
+def test_single_workgroup_cast_shares():
+    # the one-workgroup cast spreads n pairs over its 16 wavefronts in trips
+    # of 64 positions (ceil(n / 1024) trips each): one trip, trips that leave
+    # the last wavefronts empty or part full, and every trip count up to 8
+    for n in (1, 63, 64, 65, 1023, 1024, 1025, 2047, 3000, 4097, 5120, 6143, 7169):
+        a = n // 3
+        check(f"n={n}", [700, 90000], [a, n - a], bags_per_table=5, seed=100 + n)
+
+
 def sparse_bags_case(num_tables, bags_per_table, pairs_per_table, rows, seed):
     """Bags mostly without pairs: each table's pairs sit in every 4th bag,
     so a 2048-pair sort tile spans about 8192 bags (more than the pair build
