@@ -17,6 +17,15 @@ TOL = 1e-5  # max relative error of fp32 outputs, row-normwise
 # at least SPLIT_PAIRS pairs inside the workspace's cover are cut into
 # min(MAX_PIECES, len // PIECE_MIN) pieces of consecutive pairs.
 SPLIT_PAIRS, PIECE_MIN, MAX_PIECES = 2048, 1024, 32
+# The backward with a workspace sums no segment of SPLIT_PAIRS pairs or more
+# as one chain: its chains stay within about 7e-6 of the exact sum (and of
+# its square), its pieces within about 2e-6 (tests/test_summation_order.py).
+# Without a workspace (or past its cover) a longer segment is one ordered
+# fp32 chain, the literal sequential sum, which can itself miss 1e-5 against
+# the exact sum (a 9000-term chain of heavily repeated terms by 1.2e-5, the
+# 30.8k-term hottest row of the 8x5M workload by 1.4e-5 on G and 2.5e-5 on
+# G*G): such rows are checked bit for bit against the fp32 oracle only.
+FP32_CHAIN_LIMIT = SPLIT_PAIRS
 
 
 def rel_err_rows(got: np.ndarray, ref: np.ndarray) -> float:
@@ -156,26 +165,36 @@ def split_rows(orc: oracle.Oracle, cast: dict, grad_out: np.ndarray, coal: np.nd
 
 
 class OracleModel:
-    """The fp32 oracle's state over a row set (the rows the steps touch).
-    With split_cap > 0 the coalesced rows of segments the backward splits
-    take the documented piecewise order (the oracle's sums, composed)."""
+    """The oracle's state over a row set (the rows the steps touch).
+
+    precision "f32": the fp32 oracle, the same sequential algorithm in the
+    arithmetic the kernels use; with split_cap > 0 the coalesced rows of
+    segments the backward splits take the documented piecewise order (the
+    oracle's sums, composed), so the GPU must match it bit for bit.
+    precision "f64": the definition itself (sums, then the optimizer step, in
+    double from the same fp32 inputs and constants); the GPU must lie within
+    the 1e-5 row-normwise tolerance of it (split_cap is ignored)."""
 
     def __init__(self, w: wl.Workload, row_ids: np.ndarray, table_vals: np.ndarray | None = None,
-                 split_cap: int = 0):
+                 split_cap: int = 0, precision: str = "f32"):
         self.w = w
-        self.split_cap = split_cap
-        self.orc = oracle.Oracle("f32")
+        self.orc = oracle.Oracle(precision)
+        self.split_cap = split_cap if precision == "f32" else 0
         self.ids = np.asarray(row_ids, np.int64)
-        self.table = (wl.table_rows(w, self.ids) if table_vals is None
-                      else np.array(table_vals, np.float32, copy=True))
+        init = (wl.table_rows(w, self.ids) if table_vals is None
+                else np.asarray(table_vals, np.float32))
+        self.table = np.array(init, self.orc.dtype, copy=True)
         if w.optimizer in ("adagrad", "rmsprop"):
             self.acc = np.zeros_like(self.table)
         elif w.optimizer == "rowwise_adagrad":
-            self.acc = np.zeros(len(self.ids), np.float32)
+            self.acc = np.zeros(len(self.ids), self.orc.dtype)
         else:
             self.acc = None
 
-    def step(self, b: wl.Batch):
+    def step(self, b: wl.Batch, coal_override: np.ndarray | None = None):
+        """One step. coal_override: apply the update with these coalesced rows
+        (in the cast's row order) instead of the oracle's own sums -- the
+        optimizer step of the definition evaluated at another G."""
         w, o = self.w, self.orc
         src, dst = o.pairs_from_csr(w.num_tables, w.batch, b.table_row_offset, b.indices,
                                     b.bag_offsets)
@@ -183,6 +202,9 @@ class OracleModel:
         cast = o.tensor_casting(src, dst)
         coal, rows = o.coalesce(src, o.expand(dst, b.grad_out))
         self.split = split_rows(o, cast, b.grad_out, coal, self.split_cap)
+        if coal_override is not None:
+            assert coal_override.shape == coal.shape
+            coal = np.array(coal_override, o.dtype)
         scatter(o, w, rows, coal, self.table, self.acc, self.ids)
         return out, cast, coal, rows
 
@@ -204,6 +226,83 @@ def scatter(o: oracle.Oracle, w: wl.Workload, rows, coal, table, acc, ids):
         o.scatter_rowwise_adagrad(rows, coal, lr, eps, table, acc, ids)
     else:
         raise ValueError(w.optimizer)
+
+
+def check_step_against_definition(cast: dict, split, out, out64, coal, coal64,
+                                  what: str) -> np.ndarray:
+    """One step's outputs against the fp64 definition within 1e-5
+    row-normwise: forward rows against the fp64 sums over the same table
+    values (out64 from a shadow model that follows the GPU's updates), and
+    coalesced rows against the fp64 sums, except rows summed as one fp32
+    chain of FP32_CHAIN_LIMIT pairs or more (not in `split`, the split rows'
+    indices). Returns the table rows of those long chains."""
+    lens = np.diff(cast["seg_offsets"])
+    long_chain = lens >= FP32_CHAIN_LIMIT
+    long_chain[np.asarray(split, np.int64)] = False
+    assert_close(out, out64, f"{what}: forward rows vs fp64 sums")
+    assert_close(coal[~long_chain], coal64[~long_chain],
+                 f"{what}: coalesced gradient vs fp64 sums")
+    return np.asarray(cast["unique_rows"], np.int64)[long_chain]
+
+
+def check_against_definition(run: "GpuRun", model64: "OracleModel", shadow64: "OracleModel",
+                             what: str, exclude=()):
+    """The GPU's updated table and accumulator rows against the fp64
+    definition, after the same steps, within the 1e-5 row-normwise tolerance:
+
+    - accumulator rows (sums of squared coalesced gradients) against
+      model64, the definition itself;
+    - table rows against shadow64, the definition's optimizer step evaluated
+      at the GPU's own coalesced rows (each step's G must itself lie within
+      the tolerance of the fp64 sums, which the caller checks): the update
+      arithmetic, step after step;
+    - for SGD, whose step is linear in G, table rows against model64 too.
+    (For Adagrad and RMSprop the step's slope in G reaches lr/sqrt(eps) at
+    G = 0, so an element whose exact G is near 0 can move by far more than
+    1e-5 of its row under any fp32 summation of G; see check_step_slope.)
+    exclude: table rows left out of the comparisons with model64 (rows that
+    were summed as one long fp32 chain, see check_step_against_definition)."""
+    ids = model64.ids
+    got_w = run.rows(ids)
+    assert_close(got_w, shadow64.table, f"{what}: updated rows vs fp64 step at the GPU's G")
+    keep = ~np.isin(ids, np.asarray(exclude, np.int64))
+    if model64.w.optimizer == "sgd":
+        assert_close(got_w[keep], model64.table[keep], f"{what}: updated rows vs fp64 definition")
+    if model64.acc is not None:
+        got = run.acc_rows(ids).reshape(len(ids), -1)
+        assert_close(got[keep], model64.acc.reshape(len(ids), -1)[keep],
+                     f"{what}: accumulator vs fp64 definition")
+
+
+def step_slope(w: wl.Workload, g: np.ndarray, a0: np.ndarray | float = 0.0) -> np.ndarray:
+    """|dW/dG| of one optimizer step at coalesced gradient g from accumulator
+    a0 (fp64, elementwise): lr for SGD; for Eq. 2 (Adagrad: keep 1, c 1) and
+    Eq. 1 (RMSprop: keep gamma, c 1 - gamma), W' = W - lr*G/sqrt(eps +
+    keep*a0 + c*G^2), whose slope is lr*(eps + keep*a0)/(eps + keep*a0 +
+    c*G^2)^(3/2)."""
+    lr, eps, gamma = (float(np.float32(w.lr)), float(np.float32(w.eps)),
+                      float(np.float32(w.gamma)))
+    g = np.asarray(g, np.float64)
+    if w.optimizer == "sgd":
+        return np.full_like(g, lr)
+    keep, c = (1.0, 1.0) if w.optimizer == "adagrad" else (gamma, 1.0 - gamma)
+    base = eps + keep * np.asarray(a0, np.float64)
+    return lr * base / (base + c * g * g) ** 1.5
+
+
+def check_step_slope(got_w: np.ndarray, ref_w: np.ndarray, slope: np.ndarray,
+                     g_ref: np.ndarray, what: str):
+    """Table rows after one step against the fp64 definition, allowing what
+    the tolerance on G allows: per element, |got - ref| <= TOL*max|ref_row| +
+    slope*TOL*max|g_row| (the definition's step moved, to first order, by a
+    coalesced gradient within TOL row-normwise of the exact one)."""
+    got_w, ref_w = np.asarray(got_w, np.float64), np.asarray(ref_w, np.float64)
+    g_ref = np.asarray(g_ref, np.float64)
+    bound = (TOL * np.abs(ref_w).max(axis=1, keepdims=True)
+             + slope * TOL * np.abs(g_ref).max(axis=1, keepdims=True))
+    bad = np.abs(got_w - ref_w) > bound
+    assert not bad.any(), (f"{what}: {np.count_nonzero(bad)} elements beyond the tolerance "
+                           f"carried through the optimizer step")
 
 
 def compare_cast(got: dict, ref: dict, n: int):

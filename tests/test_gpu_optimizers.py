@@ -3,12 +3,15 @@ through tc_sparse_update and through the fused tc_embed_backward_update, and
 row-wise Adagrad through tc_sparse_update, over three steps so that the
 accumulator's history enters the result. Tables and accumulators must match
 the fp32 oracle bit for bit (both sides take the same separately rounded
-fp32 operations in the same order)."""
+fp32 operations in the same order), and lie within 1e-5 row-normwise of the
+fp64 definition (accumulators: the fp64 pipeline; tables: the fp64 steps at
+the GPU's coalesced rows)."""
 import numpy as np
 import pytest
 
 from paper_2010_13100_amd import workload as wl
-from tests.gpu_harness import GpuRun, OracleModel, assert_close
+from tests.gpu_harness import (GpuRun, OracleModel, assert_close, check_against_definition,
+                               check_step_against_definition)
 
 pytestmark = pytest.mark.gpu
 
@@ -27,15 +30,22 @@ def run_steps(w, fused, steps=3):
           f"{[b.num_pairs for b in batches]} touched {len(touched)}", flush=True)
     run = GpuRun(w, max_pairs=max(b.num_pairs for b in batches))
     model = OracleModel(w, touched)
+    model64 = OracleModel(w, touched, precision="f64")
+    shadow64 = OracleModel(w, touched, precision="f64")
+    chains = []
     for b in batches:
         out, cast, coal = run.step(b, fused=fused)
         _, r_cast, r_coal, r_rows = model.step(b)
+        _, _, coal64, _ = model64.step(b)
+        out64, _, _, _ = shadow64.step(b, coal_override=coal)
         assert np.array_equal(cast["unique_rows"], r_rows)
         assert_close(coal, r_coal, "coalesced gradient", bitwise=True)
+        chains.append(check_step_against_definition(cast, [], out, out64, coal, coal64, w.name))
     assert_close(run.rows(touched), model.table, "updated table rows", bitwise=True)
     acc = run.acc_rows(touched)
     assert_close(acc.reshape(len(touched), -1), model.acc.reshape(len(touched), -1),
                  f"{w.optimizer} accumulator", bitwise=True)
+    check_against_definition(run, model64, shadow64, w.name, np.concatenate(chains))
     rng = np.random.default_rng(1)
     untouched = np.setdiff1d(rng.integers(0, w.total_rows, size=4000), touched)
     assert np.array_equal(run.rows(untouched), wl.table_rows(w, untouched))
