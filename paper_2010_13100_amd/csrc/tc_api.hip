@@ -17,6 +17,23 @@ void set_error(const char *fmt, ...) {
 
 void clear_error() { g_error[0] = '\0'; }
 
+int device_cus() {
+    constexpr int kMaxDevices = 64;
+    static int cached[kMaxDevices] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+    if (dev < kMaxDevices) {
+        const int c = __atomic_load_n(&cached[dev], __ATOMIC_RELAXED);
+        if (c > 0) return c;
+    }
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus < 1)
+        return 256;
+    if (dev < kMaxDevices) __atomic_store_n(&cached[dev], cus, __ATOMIC_RELAXED);
+    return cus;
+}
+
 tc_status check_launch(const char *what) {
     const hipError_t e = hipGetLastError();
     if (e == hipSuccess) return TC_OK;

@@ -252,10 +252,13 @@ __device__ void long_producer(LongLds &lds, __amdgpu_buffer_rsrc_t id_rsrc, int3
     const int32_t col4 = (lane % kLanesPerRow) * 4;  // first of the lane's 4 columns
     const int32_t lane_bytes = part_bytes + col4 * 4;
     int32_t *offs = lds.offs[P];
-    // ids of chunk c, one per lane (0 past the end of the segment; such rows
-    // get kOutOfRange below)
+    // ids of chunk c, one per lane. The whole byte offset goes in the
+    // vector offset, which the buffer's range check covers (the scalar
+    // offset is not checked): ids past the end of the segment read as 0
+    // without touching memory, and such rows get kOutOfRange below.
     auto load_ids = [&](int32_t c) -> int32_t {
-        return __builtin_amdgcn_raw_buffer_load_b32(id_rsrc, lane * 4, c * (kChunkRows * 4), 0);
+        return __builtin_amdgcn_raw_buffer_load_b32(id_rsrc, c * (kChunkRows * 4) + lane * 4, 0,
+                                                    0);
     };
     int32_t iv[kIdAhead];
     float4 d[kAhead][L];
@@ -403,11 +406,12 @@ __device__ __forceinline__ float run_chain(LongLds &lds, const float *__restrict
         const int32_t last = __builtin_amdgcn_readfirstlane(sid[len - 1]);
         span = uint64_t(last - first + 1) * uint64_t(row_bytes);
     }
-    if (span > uint64_t(kOutOfRange) || len >= (1 << 29)) {
+    if (span > uint64_t(kOutOfRange) || len >= (1 << 28)) {
         // rows spread over about 2 GiB or more, so that kOutOfRange would not
-        // be past them (or a segment too long for 32-bit byte offsets of its
-        // ids): the consumer alone, with 64-bit addressed loads (no barriers
-        // on this path)
+        // be past them (or a segment so long that the byte offsets of its ids
+        // and of the id chunks read ahead would not stay below 2^31): the
+        // consumer alone, with 64-bit addressed loads (no barriers on this
+        // path)
         float acc = 0.f;
         if (w == 0) {
             const float *colp = grad + (col < dim ? col : dim - 1);
@@ -688,7 +692,7 @@ tc_status launch_expand(const float *grad, int32_t dim, const int32_t *bag_offse
                         int64_t num_bags, float *expanded, hipStream_t stream) {
     const RowShape s = row_shape(dim);
     const int64_t rows_per_block = (kBlock / kWave) * (kWave / s.lanes);
-    const unsigned grid = grid_for(num_bags, rows_per_block, int64_t(kNumCUs) * 8);
+    const unsigned grid = grid_for(num_bags, rows_per_block, int64_t(device_cus()) * 8);
 #define TC_EXP_CASE(L, C)                                                                    \
     if (s.lanes == L && s.chunks == C) {                                                     \
         k_expand<L, C><<<grid, kBlock, 0, stream>>>(grad, dim, bag_offsets, num_bags,        \
@@ -755,19 +759,24 @@ SplitWs make_split_ws(void *ws, size_t bytes, int32_t dim) {
     return s;
 }
 
-// Workgroups of k_backward_list: as many as can be resident at once.
+// Workgroups of k_backward_list: as many as can be resident at once on the
+// current device (occupancy query, cached per device).
 int list_blocks() {
-    static int blocks = 0;
-    if (blocks == 0) {
-        int per_cu = 0, cus = 0, dev = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_backward_list, kLongThreads,
-                                                         0) != hipSuccess ||
-            per_cu < 1 || cus < 1)
-            return kNumCUs;
-        blocks = per_cu * cus;
+    constexpr int kMaxDevices = 64;
+    static int cached[kMaxDevices] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return device_cus();
+    if (dev < kMaxDevices) {
+        const int c = __atomic_load_n(&cached[dev], __ATOMIC_RELAXED);
+        if (c > 0) return c;
     }
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_backward_list, kLongThreads,
+                                                     0) != hipSuccess ||
+        per_cu < 1)
+        return device_cus();
+    const int blocks = per_cu * device_cus();
+    if (dev < kMaxDevices) __atomic_store_n(&cached[dev], blocks, __ATOMIC_RELAXED);
     return blocks;
 }
 
@@ -787,7 +796,7 @@ tc_status launch_backward(const float *grad, int64_t grad_rows, int32_t dim,
     // the short kernel first: it builds the lists
     const RowShape s = row_shape(dim);
     const int64_t rows_per_block = (kBlock / kWave) * (kWave / s.lanes);
-    const unsigned grid = grid_for(cap, rows_per_block, int64_t(kNumCUs) * 8);
+    const unsigned grid = grid_for(cap, rows_per_block, int64_t(device_cus()) * 8);
     bool launched = false;
 #define TC_BWD_CASE(L, C)                                                                    \
     if (!launched && s.lanes == L && s.chunks == C) {                                        \
@@ -855,6 +864,45 @@ extern "C" tc_status tc_embed_backward(const float *grad_out, int32_t num_bags, 
                            stream);
 }
 
+namespace tc {
+
+namespace {
+
+// Argument checks of the backward + update entry point (`what` names the
+// caller in messages).
+tc_status check_backward_update(const char *what, const float *grad_out, int32_t num_bags,
+                                int32_t dim, const int32_t *seg_offsets,
+                                const int32_t *casted_src, const int32_t *unique_rows,
+                                const int32_t *num_unique, int64_t max_unique, const float *W,
+                                const float *opt_state, int64_t total_rows, int32_t opt_kind,
+                                float gamma, const float *coal_grad) {
+    TC_REQUIRE(num_bags >= 0 && max_unique >= 0 && total_rows >= 0, TC_ERR_INVALID_ARG,
+               "%s: negative size", what);
+    TC_REQUIRE(max_unique < (int64_t(1) << 31) && total_rows < (int64_t(1) << 31),
+               TC_ERR_INVALID_ARG, "%s: sizes must be below 2^31", what);
+    TC_REQUIRE(dim > 0 && dim % 4 == 0 && dim <= kMaxDim, TC_ERR_UNSUPPORTED,
+               "%s: dim %d must be a multiple of 4 in [4, %d]", what, dim, kMaxDim);
+    TC_REQUIRE(opt_kind >= TC_OPT_SGD && opt_kind <= TC_OPT_ROWWISE_ADAGRAD, TC_ERR_INVALID_ARG,
+               "%s: unknown optimizer %d", what, opt_kind);
+    TC_REQUIRE(opt_kind != TC_OPT_ROWWISE_ADAGRAD, TC_ERR_UNSUPPORTED,
+               "%s: row-wise Adagrad needs whole rows; use tc_embed_backward and "
+               "tc_sparse_update", what);
+    TC_REQUIRE((opt_kind == TC_OPT_SGD) == (opt_state == nullptr), TC_ERR_INVALID_ARG,
+               "%s: opt_state must be NULL for SGD and given otherwise", what);
+    TC_REQUIRE(opt_kind != TC_OPT_RMSPROP || (gamma >= 0.f && gamma <= 1.f), TC_ERR_INVALID_ARG,
+               "%s: RMSprop gamma must lie in [0, 1]", what);
+    if (max_unique == 0) return TC_OK;
+    TC_REQUIRE(grad_out && seg_offsets && casted_src && unique_rows && num_unique && W,
+               TC_ERR_INVALID_ARG, "%s: null pointer", what);
+    TC_REQUIRE(aligned16(grad_out) && aligned16(W) && (!opt_state || aligned16(opt_state)) &&
+                   (!coal_grad || aligned16(coal_grad)),
+               TC_ERR_UNSUPPORTED, "%s: float pointers must be 16-byte aligned", what);
+    return TC_OK;
+}
+
+}  // namespace
+}  // namespace tc
+
 extern "C" tc_status tc_embed_backward_update(
     const float *grad_out, int32_t num_bags, int32_t dim, const int32_t *seg_offsets,
     const int32_t *casted_src, const int32_t *unique_rows, const int32_t *num_unique,
@@ -862,29 +910,11 @@ extern "C" tc_status tc_embed_backward_update(
     float lr, float eps, float gamma, float *coal_grad, void *workspace, size_t workspace_bytes,
     hipStream_t stream) {
     clear_error();
-    TC_REQUIRE(num_bags >= 0 && max_unique >= 0 && total_rows >= 0, TC_ERR_INVALID_ARG,
-               "tc_embed_backward_update: negative size");
-    TC_REQUIRE(max_unique < (int64_t(1) << 31) && total_rows < (int64_t(1) << 31),
-               TC_ERR_INVALID_ARG, "tc_embed_backward_update: sizes must be below 2^31");
-    TC_REQUIRE(dim > 0 && dim % 4 == 0 && dim <= kMaxDim, TC_ERR_UNSUPPORTED,
-               "tc_embed_backward_update: dim %d must be a multiple of 4 in [4, %d]", dim,
-               kMaxDim);
-    TC_REQUIRE(opt_kind >= TC_OPT_SGD && opt_kind <= TC_OPT_ROWWISE_ADAGRAD, TC_ERR_INVALID_ARG,
-               "tc_embed_backward_update: unknown optimizer %d", opt_kind);
-    TC_REQUIRE(opt_kind != TC_OPT_ROWWISE_ADAGRAD, TC_ERR_UNSUPPORTED,
-               "tc_embed_backward_update: row-wise Adagrad needs whole rows; use "
-               "tc_embed_backward and tc_sparse_update");
-    TC_REQUIRE((opt_kind == TC_OPT_SGD) == (opt_state == nullptr), TC_ERR_INVALID_ARG,
-               "tc_embed_backward_update: opt_state must be NULL for SGD and given otherwise");
-    TC_REQUIRE(opt_kind != TC_OPT_RMSPROP || (gamma >= 0.f && gamma <= 1.f), TC_ERR_INVALID_ARG,
-               "tc_embed_backward_update: RMSprop gamma must lie in [0, 1]");
-    if (max_unique == 0) return TC_OK;
-    TC_REQUIRE(grad_out && seg_offsets && casted_src && unique_rows && num_unique && W,
-               TC_ERR_INVALID_ARG, "tc_embed_backward_update: null pointer");
-    TC_REQUIRE(aligned16(grad_out) && aligned16(W) && (!opt_state || aligned16(opt_state)) &&
-                   (!coal_grad || aligned16(coal_grad)),
-               TC_ERR_UNSUPPORTED,
-               "tc_embed_backward_update: float pointers must be 16-byte aligned");
+    const tc_status st = check_backward_update(
+        "tc_embed_backward_update", grad_out, num_bags, dim, seg_offsets, casted_src,
+        unique_rows, num_unique, max_unique, W, opt_state, total_rows, opt_kind, gamma,
+        coal_grad);
+    if (st != TC_OK || max_unique == 0) return st;
     TC_REQUIRE(workspace_bytes == 0 || (workspace && aligned16(workspace)), TC_ERR_INVALID_ARG,
                "tc_embed_backward_update: workspace must be a 16-byte aligned pointer");
     const RowSink sink{coal_grad, W, opt_state, unique_rows, opt_kind, lr, eps, gamma,

@@ -1027,7 +1027,7 @@ tc_status cast_impl(const char *what, bool positions, const int64_t *table_row_o
         unsigned fb = 0;
         if (fl) {
             const int64_t per_block = int64_t(kSmallThreads / kWave) * (kWave / fl);
-            fb = grid_for(num_bags, per_block, kNumCUs - 1);
+            fb = grid_for(num_bags, per_block, device_cus() > 1 ? device_cus() - 1 : 1);
         }
         const FwdSlice fs = fl ? *fwd : FwdSlice{};
 #define TC_SMALL(FL)                                                                         \
@@ -1068,7 +1068,7 @@ tc_status cast_impl(const char *what, bool positions, const int64_t *table_row_o
         // the tiles' pair builds, then the forward's workgroups, in one launch
         const int64_t per_block = int64_t(kBlock / kWave) * (kWave / fl);
         const unsigned grid =
-            unsigned(sort_tiles) + grid_for(num_bags, per_block, int64_t(kNumCUs) * 32);
+            unsigned(sort_tiles) + grid_for(num_bags, per_block, int64_t(device_cus()) * 32);
 #define TC_FWD_BUILD(FL)                                                                     \
     k_forward_build<FL><<<grid, kBlock, 0, stream>>>(*fwd, num_tables, int32_t(num_pairs),    \
                                                      local, recs, sort_tiles, ka, va, counts,  \
@@ -1080,7 +1080,7 @@ tc_status cast_impl(const char *what, bool positions, const int64_t *table_row_o
         tc_status st = check_launch("k_forward_build");
         if (st != TC_OK) return st;
     } else {
-        const unsigned grid = grid_for(num_bags, kBlock / 16, int64_t(kNumCUs) * 8);
+        const unsigned grid = grid_for(num_bags, kBlock / 16, int64_t(device_cus()) * 8);
         k_build_keys<<<grid, kBlock, 0, stream>>>(indices, bag_offsets, table_row_offset,
                                                   num_bags, bags_per_table, num_tables, local,
                                                   positions, recs, sort_tiles, ka, va);

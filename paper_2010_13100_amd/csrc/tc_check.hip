@@ -147,7 +147,7 @@ extern "C" tc_status tc_check_index(const int64_t *table_row_offset, int32_t num
     int64_t items = num_pairs;
     if (num_bags + 1 > items) items = num_bags + 1;
     if (int64_t(num_tables) + 1 > items) items = int64_t(num_tables) + 1;
-    const unsigned grid = grid_for(items, int64_t(kBlock) * 4, int64_t(kNumCUs) * 8);
+    const unsigned grid = grid_for(items, int64_t(kBlock) * 4, int64_t(device_cus()) * 8);
     k_check_index<<<grid, kBlock, 0, stream>>>(table_row_offset, num_tables, bags_per_table,
                                                total_rows, max_table_rows, indices, bag_offsets,
                                                num_pairs, report);

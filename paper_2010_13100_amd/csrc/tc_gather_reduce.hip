@@ -38,7 +38,7 @@ tc_status launch_forward(const float *W, int32_t dim, const int32_t *ids, const 
     const int64_t rows_per_block = (kBlock / kWave) * (kWave / s.lanes);
     // up to 32 workgroups per CU in the grid (8 are resident at a time): on
     // 33 GB tables the random row reads finish about 3% sooner than with 8
-    const unsigned grid = grid_for(num_bags, rows_per_block, int64_t(kNumCUs) * 32);
+    const unsigned grid = grid_for(num_bags, rows_per_block, int64_t(device_cus()) * 32);
     const FwdSlice f{W, ids, offsets, table_row_offset, out, 0, num_bags, dim, bags_per_table};
 #define TC_FWD_CASE(L, C)                                                                      \
     if (s.lanes == L && s.chunks == C) {                                                       \

@@ -19,8 +19,12 @@ tc_status check_launch(const char *what);
 
 constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kBlock = 256;        // threads per block for the streaming kernels
-constexpr int kNumCUs = 256;       // MI355X compute units
 constexpr int kMaxDim = 1024;
+
+// Compute units of the current device (hipDeviceGetAttribute, cached per
+// device; 256, an MI355X's count, if the query fails). Grids are sized in
+// workgroups per CU from it.
+int device_cus();
 
 inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 

@@ -124,7 +124,7 @@ tc_status launch_update(float *W, float *A, int32_t dim, const int32_t *rows, co
                         float gamma, hipStream_t stream) {
     const RowShape s = row_shape(dim);
     const int64_t rows_per_block = (kBlock / kWave) * (kWave / s.lanes);
-    const unsigned grid = grid_for(cap, rows_per_block, int64_t(kNumCUs) * 8);
+    const unsigned grid = grid_for(cap, rows_per_block, int64_t(device_cus()) * 8);
 #define TC_UP_CASE(L, C)                                                                 \
     if (s.lanes == L && s.chunks == C) {                                                 \
         k_sparse_update<L, C, OPT><<<grid, kBlock, 0, stream>>>(                          \
