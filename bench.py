@@ -8,10 +8,14 @@ pass), back to back on one stream, with inputs already resident in HBM.
 --unfused makes every step a separate call (tc_embed_forward, tc_cast_index,
 tc_embed_backward, tc_sparse_update). Prints ONE JSON line.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config c2] [--no-overlap] [--unfused]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config c4] [--also c3,c5,c2,c1]
+                  [--no-overlap] [--unfused]
 
-Default workload: 8 tables x 1M rows x 64 fp32, batch 2048, 80 Zipf(1.05)
-indices per bag, SGD (configuration "c2"). Other configurations: c1..c5.
+The headline workload (--config, default c4) is the largest one that fits
+one GPU: 32 tables x 1M rows x 256 fp32, batch 8192, 20 uniform indices per
+bag, SGD. The line also carries compact results (steps/s, per-call times,
+HBM fractions, longest segment) for the workloads named by --also, timed
+the same way, each after the previous one's memory is freed.
 """
 from __future__ import annotations
 
@@ -28,8 +32,9 @@ NUM_BATCHES = 4        # distinct pre-generated batches the timed steps cycle th
 
 
 def algorithmic_bytes(w, n, u, nbags):
-    """Bytes each call must move at minimum under the paper's analytic model
-    (every gather counted once, Sec. III-C): index reads, row reads, row writes."""
+    """Bytes each call moves under the paper's analytic model (every gather
+    counted once, Sec. III-C): index reads, one row read per gather, row
+    writes."""
     D4 = 4 * w.dim
     fwd = n * 4 + (nbags + 1) * 4 + n * D4 + nbags * D4
     cast = n * 4 + (nbags + 1) * 4 + n * 4 + u * 4 + (u + 1) * 4
@@ -41,6 +46,37 @@ def algorithmic_bytes(w, n, u, nbags):
     fused = n * 4 + (u + 1) * 4 + n * D4 + u * 4 + (rows_rw - 1) * u * D4
     return {"forward": fwd, "cast": cast, "backward": bwd, "update": upd,
             "backward_update": fused, "forward_cast": fwd + cast}
+
+
+def compulsory_bytes(w, n, u, nbags):
+    """A lower bound per call: as algorithmic_bytes, but every distinct row a
+    call gathers is read once (the forward's U table rows, the backward's
+    T*B output-gradient rows), as a perfect cache would give."""
+    D4 = 4 * w.dim
+    a = algorithmic_bytes(w, n, u, nbags)
+    fwd = a["forward"] - n * D4 + u * D4
+    bwd_saved = n * D4 - nbags * D4
+    return {"forward": fwd, "cast": a["cast"], "backward": a["backward"] - bwd_saved,
+            "update": a["update"], "backward_update": a["backward_update"] - bwd_saved,
+            "forward_cast": fwd + a["cast"]}
+
+
+def host_cpu():
+    """Model name and usable core count of the host CPU."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = os.cpu_count()
+    return {"cpu_model": model, "nproc": usable, "os_cpu_count": os.cpu_count()}
 
 
 # Sources of each call's kernels, and the kernels one call launches.
@@ -149,15 +185,19 @@ def run_ab(args, w, trainer, dbat, stream):
 
 
 def write_traffic(pmc_dir: str, workload: str, calls) -> dict:
-    """Turn four rocprofv3 --pmc CSV runs into HBM bytes per call launch and
-    store them in profiles/traffic.json under "<call>:<workload>".
+    """Turn rocprofv3 --pmc CSV runs into HBM bytes per call launch and store
+    them in profiles/traffic.json under "<call>:<workload>".
 
     pmc_dir holds copy_fetch/, copy_write/ (bench.py --copy-calibration runs)
-    and fetch/, write/ (runs of this workload), each with the
-    run_counter_collection.csv that `rocprofv3 --pmc FETCH_SIZE|WRITE_SIZE -f csv
-    -o run` writes. FETCH_SIZE and WRITE_SIZE are KiB per dispatch; each is
-    scaled by copy_bytes / counter-reading-for-the-copy, the counter's own error
-    on a plain device copy of known size."""
+    and fetch/, write/ (runs of `bench.py --profile-steps` on this workload,
+    which launch the step's calls and nothing else of the library), each with
+    the run_counter_collection.csv that `rocprofv3 --pmc FETCH_SIZE|WRITE_SIZE
+    -f csv -o run` writes, plus `steps` (step runs in the profiled program)
+    and `copy_bytes`. FETCH_SIZE and WRITE_SIZE are KiB per dispatch; each is
+    scaled by copy_bytes / counter-reading-for-the-copy, the counter's own
+    error on a plain device copy of known size. A call's bytes per launch
+    are the scaled bytes of all dispatches of its kernels over the number of
+    steps."""
     import csv
     import re
 
@@ -172,33 +212,32 @@ def write_traffic(pmc_dir: str, workload: str, calls) -> dict:
         return out
 
     scale = {}
+    bytes_per_copy = int(open(os.path.join(pmc_dir, "copy_bytes")).read())
     for sub, counter in (("copy_fetch", "FETCH_SIZE"), ("copy_write", "WRITE_SIZE")):
         copies = [float(r["Counter_Value"]) * 1024.0 for r in rows(sub)
                   if "copyBuffer" in r["Kernel_Name"]]
-        bytes_per_copy = int(open(os.path.join(pmc_dir, "copy_bytes")).read())
         scale[counter] = bytes_per_copy / (sum(copies) / len(copies))
+    steps = int(open(os.path.join(pmc_dir, "steps")).read())
     fetch, write = per_kernel("fetch"), per_kernel("write")
     p = os.path.join(ROOT, "profiles", "traffic.json")
     table = json.load(open(p)) if os.path.exists(p) else {}
     for call in calls:
-        names = KERNEL_NAMES[call]
         fb = wb = 0.0
-        found = True
-        for k in names:
+        seen = []
+        for k in KERNEL_NAMES[call]:
             pat = re.compile(r"\b" + k + r"\b")
             fv = [v for n, vs in fetch.items() if pat.search(n) for v in vs]
             wv = [v for n, vs in write.items() if pat.search(n) for v in vs]
-            if not fv or not wv:
-                found = False
-                break
-            fb += sum(fv) / len(fv)
-            wb += sum(wv) / len(wv)
-        if not found:
+            if fv and wv:
+                seen.append(k)
+                fb += sum(fv)
+                wb += sum(wv)
+        if not seen:
             continue
-        fb *= scale["FETCH_SIZE"]
-        wb *= scale["WRITE_SIZE"]
+        fb *= scale["FETCH_SIZE"] / steps
+        wb *= scale["WRITE_SIZE"] / steps
         table[f"{call}:{workload}"] = {
-            "source_sha": source_sha(call), "kernels": names,
+            "source_sha": source_sha(call), "kernels": seen, "steps": steps,
             "fetch_bytes_per_launch": round(fb), "write_bytes_per_launch": round(wb),
             "hbm_bytes_per_launch": round(fb + wb),
             "fetch_scale": round(scale["FETCH_SIZE"], 4), "write_scale": round(scale["WRITE_SIZE"], 4)}
@@ -209,31 +248,54 @@ def write_traffic(pmc_dir: str, workload: str, calls) -> dict:
 
 
 def cpu_baseline(w, batch, budget_s: float):
-    """The fp32 oracle (single thread) on the same workload: forward, baseline
-    expand + coalesce backward, casting, update, on the rows batch 0 touches."""
+    """The fp32 oracle (single thread) on a bounded sample of the workload:
+    forward, casting, the baseline expand + coalesce backward and the update,
+    on the rows the sample touches. The sample is the first whole tables (or,
+    for one table, the first bags) holding about 84M gathered floats (a
+    1.3M-pair batch of 64-float rows, about half a second of oracle work);
+    steps/s is scaled to the full batch by its share of the pairs."""
     import numpy as np
 
     import oracle
     from paper_2010_13100_amd import workload as wl
     orc = oracle.Oracle("f32")
-    t = np.repeat(np.arange(w.num_bags) // w.batch, np.diff(batch.bag_offsets))
-    ids = np.unique(batch.table_row_offset[t] + batch.indices)
+    target_pairs = max(1, 84_000_000 // w.dim)
+    bo = batch.bag_offsets
+    if batch.num_pairs <= target_pairs:
+        tables, bags = w.num_tables, w.batch
+    elif w.num_tables > 1:
+        per_table = bo[np.arange(1, w.num_tables + 1) * w.batch] - bo[np.arange(w.num_tables)
+                                                                      * w.batch]
+        tables = max(1, int(np.searchsorted(np.cumsum(per_table), target_pairs, side="right")))
+        bags = w.batch
+    else:
+        tables, bags = 1, max(1, int(np.searchsorted(bo, target_pairs, side="right")) - 1)
+    nb = tables * bags
+    s_bo = bo[:nb + 1].copy()
+    n = int(s_bo[-1])
+    s_idx = batch.indices[:n]
+    s_off = batch.table_row_offset[:tables + 1].copy()
+    s_grad = batch.grad_out[:nb]
+    t = np.repeat(np.arange(nb) // bags, np.diff(s_bo))
+    ids = np.unique(s_off[t] + s_idx)
     table = wl.table_rows(w, ids)
     steps, t0 = 0, time.perf_counter()
     phases: dict = {}
     while True:
-        oracle.train_step(orc, num_tables=w.num_tables, bags_per_table=w.batch,
-                          table_row_offset=batch.table_row_offset, indices=batch.indices,
-                          bag_offsets=batch.bag_offsets, grad_out=batch.grad_out, table=table,
+        oracle.train_step(orc, num_tables=tables, bags_per_table=bags, table_row_offset=s_off,
+                          indices=s_idx, bag_offsets=s_bo, grad_out=s_grad, table=table,
                           table_ids=ids, optimizer=w.optimizer, lr=np.float32(w.lr),
                           eps=np.float32(w.eps), gamma=np.float32(w.gamma), timings=phases)
         steps += 1
         el = time.perf_counter() - t0
         if el >= budget_s or steps >= 50:
             break
-    return {"value": steps / el, "unit": "steps/s", "cores": 1, "kind": "oracle",
-            "sample": f"{steps} full steps of batch 0 ({batch.num_pairs} pairs), fp32 oracle, "
-                      f"table rows restricted to the {len(ids)} rows the batch touches",
+    share = n / batch.num_pairs
+    return {"value": steps / el * share, "unit": "steps/s", "cores": 1, "kind": "oracle",
+            "sample": f"{steps} oracle steps (fp32, one thread) on the first {tables} "
+                      f"table(s) x {bags} bags of batch 0: {n} of {batch.num_pairs} pairs, "
+                      f"{len(ids)} table rows; steps/s scaled by that share of the pairs",
+            "sample_steps_per_s": round(steps / el, 4),
             "seconds_per_phase": {k: round(v / steps, 4) for k, v in phases.items()}}
 
 
@@ -291,8 +353,15 @@ def measure_step(args, w, cfg_name, trainer, dbat, stream, calls, traffic_key):
     def ev_pair():
         return (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
 
+    if args.profile_steps:
+        # for profiler runs: the step calls only, nothing else on the GPU
+        for i in range(args.warmup + args.steps):
+            step(i)
+        torch.cuda.synchronize()
+        return None
+
     # warm-up steps, every call timed: per-call durations and the dominant call
-    print(f"[bench] warmup {args.warmup} steps", file=sys.stderr, flush=True)
+    print(f"[bench] {cfg_name}: warmup {args.warmup} steps", file=sys.stderr, flush=True)
     wev = [{c: ev_pair() for c in calls} for _ in range(args.warmup)]
     for i in range(args.warmup):
         step(i, wev[i])
@@ -300,10 +369,8 @@ def measure_step(args, w, cfg_name, trainer, dbat, stream, calls, traffic_key):
     skip = 1 if args.warmup > 1 else 0   # the first step also pays one-time costs
     per_call_ms = {c: float(np.mean([e[c][0].elapsed_time(e[c][1]) for e in wev[skip:]]))
                    for c in calls} if args.warmup else {c: float("nan") for c in calls}
-    # the dominant call among those with a bandwidth roofline (the cast's
-    # sort is bound by latency and arithmetic, not by HBM)
-    single = [c for c in calls if c not in ("cast", "forward_cast")]
-    dom = max(single, key=lambda c: per_call_ms[c]) if args.warmup else single[-1]
+    # the dominant call: the longest one of the step
+    dom = max(calls, key=lambda c: per_call_ms[c]) if args.warmup else calls[-1]
 
     # timed steps: start/stop around the whole region, one event pair around
     # the dominant call of each step (on the stream its kernels run on)
@@ -320,26 +387,41 @@ def measure_step(args, w, cfg_name, trainer, dbat, stream, calls, traffic_key):
     ms_total = start.elapsed_time(stop)
     ms_step = ms_total / args.steps
     dom_ms = float(np.mean([e[dom][0].elapsed_time(e[dom][1]) for e in tev]))
-    print(f"[bench] timed {args.steps} steps: {ms_step:.4f} ms/step (wall {wall:.3f} s)",
-          file=sys.stderr, flush=True)
+    print(f"[bench] {cfg_name}: timed {args.steps} steps: {ms_step:.4f} ms/step "
+          f"(wall {wall:.3f} s)", file=sys.stderr, flush=True)
 
-    # unique rows per batch (read once, outside the timed region)
-    uniq = []
+    # unique rows and longest segment per batch (outside the timed region)
+    uniq, longest = [], []
     for i in range(NUM_BATCHES):
         d = dbat[i]
         trainer.cast(d["off"], d["idx"], d["bo"], d["n"], stream)
-        uniq.append(int(trainer.num_unique.item()))
-    nbytes = {c: 0.0 for c in calls}
+        u = int(trainer.num_unique.item())
+        so = trainer.seg_offsets[:u + 1]
+        uniq.append(u)
+        longest.append(int((so[1:] - so[:-1]).max().item()) if u else 0)
+    alg = {c: 0.0 for c in calls}
+    comp = {c: 0.0 for c in calls}
     for i in range(args.steps):
         b = (args.warmup + i) % NUM_BATCHES
-        for c, v in algorithmic_bytes(w, dbat[b]["n"], uniq[b], w.num_bags).items():
-            if c in nbytes:
-                nbytes[c] += v / args.steps
-    step_bytes = sum(nbytes.values())
+        a = algorithmic_bytes(w, dbat[b]["n"], uniq[b], w.num_bags)
+        m = compulsory_bytes(w, dbat[b]["n"], uniq[b], w.num_bags)
+        for c in calls:
+            alg[c] += a[c] / args.steps
+            comp[c] += m[c] / args.steps
+    step_alg, step_comp = sum(alg.values()), sum(comp.values())
+    step_s = ms_step * 1e-3
 
-    achieved = nbytes[dom] / (dom_ms * 1e-3) / 1e9
-    traffic = None if traffic_key is None else load_traffic(dom, traffic_key)
+    counted = {c: None if traffic_key is None else load_traffic(c, traffic_key) for c in calls}
+    step_counted = (None if any(v is None for v in counted.values())
+                    else float(sum(counted.values())))
+    achieved = alg[dom] / (dom_ms * 1e-3) / 1e9
+    traffic = counted[dom]
     traffic_gbs = None if traffic is None else traffic / (dom_ms * 1e-3) / 1e9
+
+    def frac(nbytes, sec):
+        return None if nbytes is None else round(nbytes / sec / 1e9 / HBM_PEAK_GBS, 4)
+
+    call_name = {"update": "tc_sparse_update", "cast": "tc_cast_index"}
     return {
         "metric": "embedding train steps/sec (fwd+cast+bwd+update) and achieved HBM GB/s",
         "value": round(args.steps / (ms_total * 1e-3), 3),
@@ -358,25 +440,53 @@ def measure_step(args, w, cfg_name, trainer, dbat, stream, calls, traffic_key):
                    "rows_per_table": w.rows_per_table, "dim": w.dim, "batch": w.batch,
                    "pairs_per_step": round(float(np.mean([d["n"] for d in dbat])), 1),
                    "unique_rows_per_step": round(float(np.mean(uniq)), 1),
+                   "longest_segment": max(longest),
                    "optimizer": w.optimizer,
                    "step_calls": calls},
-        "step_algorithmic_GBps": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
-        "step_algorithmic_frac_of_hbm_peak": round(step_bytes / (ms_step * 1e-3) / 1e9
-                                                   / HBM_PEAK_GBS, 4),
+        # the whole step against the HBM peak, three ways: the paper's traffic
+        # model (every gather counted), the byte counters (rocprofv3
+        # FETCH_SIZE + WRITE_SIZE, scaled), and the compulsory bound (every
+        # distinct row once)
+        "step_hbm": {
+            "algorithmic_bytes": round(step_alg),
+            "algorithmic_frac": frac(step_alg, step_s),
+            "counter_bytes": None if step_counted is None else round(step_counted),
+            "counter_frac": frac(step_counted, step_s),
+            "compulsory_bytes": round(step_comp),
+            "compulsory_frac": frac(step_comp, step_s),
+            "peak_GBps": HBM_PEAK_GBS},
         "per_call_us": {c: round(v * 1e3, 2) for c, v in per_call_ms.items()},
         "per_call_us_measured_on": f"warm-up steps {skip}..{args.warmup - 1}, every call timed",
-        "per_call_algorithmic_GBps": {c: round(nbytes[c] / (per_call_ms[c] * 1e-3) / 1e9, 1)
+        "per_call_algorithmic_GBps": {c: round(alg[c] / (per_call_ms[c] * 1e-3) / 1e9, 1)
                                       for c in calls},
-        "roofline": {"bound": "hbm", "call": f"tc_embed_{dom}" if dom != "update"
-                     else "tc_sparse_update", "kernels": KERNEL_NAMES[dom],
+        "per_call_counter_GBps": {c: None if counted[c] is None
+                                  else round(counted[c] / (per_call_ms[c] * 1e-3) / 1e9, 1)
+                                  for c in calls},
+        "roofline": {"bound": "hbm", "call": call_name.get(dom, f"tc_embed_{dom}"),
+                     "kernels": KERNEL_NAMES[dom],
                      "launch_us": round(dom_ms * 1e3, 2),
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic,
                      "traffic_GBps": None if traffic_gbs is None else round(traffic_gbs, 1),
                      "traffic_frac": None if traffic_gbs is None
-                     else round(traffic_gbs / HBM_PEAK_GBS, 4)},
+                     else round(traffic_gbs / HBM_PEAK_GBS, 4),
+                     "compulsory_frac": frac(comp[dom], dom_ms * 1e-3)},
     }
+
+
+def compact(res):
+    """The fields of a side workload's result kept in the headline line."""
+    r = res["roofline"]
+    return {"workload": res["config"]["workload"], "steps_per_s": res["value"],
+            "ms_per_step": res["ms_per_step"], "per_call_us": res["per_call_us"],
+            "pairs_per_step": res["config"]["pairs_per_step"],
+            "unique_rows_per_step": res["config"]["unique_rows_per_step"],
+            "longest_segment": res["config"]["longest_segment"],
+            "step_hbm": {k: v for k, v in res["step_hbm"].items() if k.endswith("frac")},
+            "dominant_call": r["call"], "dominant_algorithmic_frac": r["frac"],
+            "dominant_counter_frac": r["traffic_frac"],
+            "dominant_compulsory_frac": r["compulsory_frac"]}
 
 
 def run_sweep(args, base, cfg_name, dev):
@@ -405,7 +515,7 @@ def run_sweep(args, base, cfg_name, dev):
             "per_call_us": res["per_call_us"],
             "dominant_call": res["roofline"]["call"],
             "dominant_frac_of_hbm_peak": res["roofline"]["frac"],
-            "step_algorithmic_frac_of_hbm_peak": res["step_algorithmic_frac_of_hbm_peak"],
+            "step_hbm": res["step_hbm"],
             "ab_baseline_us": ab["baseline_us"], "ab_casted_us": ab["casted_us"],
             "ab_speedup": ab["speedup"], "ab_bytes_ratio": ab["algorithmic_bytes"]["ratio"],
             "steps": args.steps, "warmup": args.warmup}), flush=True)
@@ -414,12 +524,38 @@ def run_sweep(args, base, cfg_name, dev):
         torch.cuda.empty_cache()
 
 
+def run_workload(args, cfg_name, dev, keep_batch=False):
+    """Set up one workload, time its step, free its device memory. Returns
+    (result line, batch 0 if keep_batch else None)."""
+    import torch
+
+    from paper_2010_13100_amd import workload as wl
+
+    w = wl.WORKLOADS[cfg_name]
+    variant = wl.variant(w, batch=args.batch, dim=args.dim, optimizer=args.optimizer)
+    traffic_key = cfg_name if variant is w and not args.no_overlap and not args.unfused else None
+    w = variant
+    batches, trainer, dbat = setup(w, dev)
+    stream = torch.cuda.current_stream(dev)
+    res = measure_step(args, w, cfg_name, trainer, dbat, stream, step_calls(args, w),
+                       traffic_key)
+    keep = batches[0] if keep_batch else None
+    del trainer, dbat, batches
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res, keep, w
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5"],
+                    help="the headline workload (default c4, the largest on one GPU)")
+    ap.add_argument("--also", default="c3,c5,c2,c1",
+                    help="workloads timed after the headline one, reported compactly in "
+                         "the same line under other_workloads ('' for none)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle work for cpu_baseline (0 disables)")
     ap.add_argument("--ab", action="store_true",
@@ -440,6 +576,10 @@ def main():
     ap.add_argument("--sweep", default=None, metavar="batch=B1,B2,..|dim=D1,D2,..",
                     help="sensitivity sweep: step and backward A/B per value, one JSON line "
                          "each, then exit")
+    ap.add_argument("--profile-steps", action="store_true",
+                    help="for profiler runs: run warmup + steps steps of --config and "
+                         "nothing else on the GPU (no events, no extra casts), print one "
+                         "line and exit")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run 5 plain device copies of BYTES bytes (scale for the HBM "
                          "byte counters) and exit")
@@ -448,8 +588,8 @@ def main():
                          "counter runs in PMC_DIR and exit (no GPU needed)")
     args = ap.parse_args()
     if args.traffic_from:
-        calls = ["forward", "backward", "update"] if args.unfused else ["forward", "backward_update"]
-        print(json.dumps(write_traffic(args.traffic_from, args.config, calls), indent=1))
+        print(json.dumps(write_traffic(args.traffic_from, args.config,
+                                       ["forward_cast", "backward_update"]), indent=1))
         return
     if args.copy_calibration:
         import torch
@@ -470,23 +610,33 @@ def main():
     from paper_2010_13100_amd import workload as wl
 
     dev = torch.device("cuda", 0)
-    w = wl.WORKLOADS[args.config]
-    variant = wl.variant(w, batch=args.batch, dim=args.dim, optimizer=args.optimizer)
-    traffic_key = args.config if variant is w else None
-    w = variant
-    if args.sweep:
-        run_sweep(args, w, args.config, dev)
+    if args.sweep or args.ab or args.profile_steps:
+        w = wl.variant(wl.WORKLOADS[args.config], batch=args.batch, dim=args.dim,
+                       optimizer=args.optimizer)
+        if args.sweep:
+            run_sweep(args, w, args.config, dev)
+            return
+        _, trainer, dbat = setup(w, dev)
+        stream = torch.cuda.current_stream(dev)
+        if args.ab:
+            print(json.dumps(run_ab(args, w, trainer, dbat, stream)), flush=True)
+        else:
+            measure_step(args, w, args.config, trainer, dbat, stream, step_calls(args, w), None)
+            print(json.dumps({"profile_steps": args.warmup + args.steps,
+                              "workload": args.config, "calls": step_calls(args, w)}),
+                  flush=True)
         return
-    batches, trainer, dbat = setup(w, dev)
-    stream = torch.cuda.current_stream(dev)
-    if args.ab:
-        print(json.dumps(run_ab(args, w, trainer, dbat, stream)), flush=True)
-        return
-    result = measure_step(args, w, args.config, trainer, dbat, stream, step_calls(args, w),
-                          traffic_key)
+
+    result, batch0, w = run_workload(args, args.config, dev, keep_batch=args.cpu_budget > 0)
+    others = [c for c in args.also.split(",") if c and c != args.config]
+    result["other_workloads"] = {}
+    for c in others:
+        res, _, _ = run_workload(args, c, dev)
+        result["other_workloads"][c] = compact(res)
+    result["host"] = host_cpu()
     if args.cpu_budget > 0:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(w, batches[0], args.cpu_budget)
+        result["cpu_baseline"] = cpu_baseline(w, batch0, args.cpu_budget)
     else:
         result["cpu_baseline"] = None
     print(json.dumps(result), flush=True)
