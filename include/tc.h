@@ -31,8 +31,9 @@
  * "host". The library never allocates or frees device memory, never
  * synchronises the stream and never copies to the host; scratch memory comes
  * from the caller's workspaces (tc_cast_workspace_bytes,
- * tc_backward_workspace_bytes). Buffers must stay alive until the stream has
- * finished the call.
+ * tc_backward_workspace_bytes), or, for tc_embed_backward_update_noalloc,
+ * from a fixed array the library holds in device memory. Buffers must stay
+ * alive until the stream has finished the call.
  *
  * Every call is asynchronous on `stream` (a hipStream_t; NULL is the legacy
  * default stream) and returns a tc_status. Host-side argument checks run
@@ -81,7 +82,7 @@
 extern "C" {
 #endif
 
-#define TC_ABI_VERSION 6
+#define TC_ABI_VERSION 7
 
 /* Segments at least this long are summed in pieces when a backward
  * workspace covers them (tc_embed_backward). */
@@ -310,6 +311,41 @@ tc_status tc_embed_backward_update(const float *grad_out, int32_t num_bags, int3
                                    int64_t total_rows, int32_t opt_kind, float lr, float eps,
                                    float gamma, float *coal_grad, void *workspace,
                                    size_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of the fixed device scratch of tc_embed_backward_update_noalloc
+ * (one copy per GPU the library runs that call on). */
+#define TC_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+
+/*
+ * tc_embed_backward_update for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same computation, kernels and results bit for bit as
+ * tc_embed_backward_update given a workspace that covers the step, but the
+ * backward workspace is a fixed array of TC_NOALLOC_SCRATCH_BYTES in device
+ * memory that the library holds, one per GPU, from the first use on that
+ * GPU until the process ends. The call allocates and frees nothing.
+ *   num_pairs  pairs of the step (seg_offsets[*num_unique]). The call
+ *              returns TC_ERR_WORKSPACE, launching nothing, when
+ *              tc_backward_workspace_bytes(num_pairs, dim) exceeds
+ *              TC_NOALLOC_SCRATCH_BYTES (it covers up to 35.8M pairs at
+ *              dim 64, 13.7M at dim 256, 3.9M at dim 1024).
+ * Other arguments and checks are those of tc_embed_backward_update.
+ * Every call on one GPU uses that GPU's one scratch array, which keeps the
+ * last call's contents (the call itself clears what must start at zero):
+ * calls that overlap on one GPU (different streams, or different threads
+ * without ordering) race and give undefined results; calls in stream order
+ * on one stream are safe. The first call on a GPU looks the array's address
+ * up (hipGetSymbolAddress) and may return TC_ERR_HIP if that fails.
+ */
+tc_status tc_embed_backward_update_noalloc(const float *grad_out, int32_t num_bags, int32_t dim,
+                                           const int32_t *seg_offsets,
+                                           const int32_t *casted_src,
+                                           const int32_t *unique_rows,
+                                           const int32_t *num_unique, int64_t max_unique,
+                                           int64_t num_pairs, float *W, float *opt_state,
+                                           int64_t total_rows, int32_t opt_kind, float lr,
+                                           float eps, float gamma, float *coal_grad,
+                                           hipStream_t stream);
 
 /* What tc_check_index found (report[0]). */
 typedef enum tc_index_problem {

@@ -866,10 +866,18 @@ extern "C" tc_status tc_embed_backward(const float *grad_out, int32_t num_bags, 
 
 namespace tc {
 
+// The no-allocation entry point's backward workspace: a fixed array in
+// device memory, one copy per GPU, held until the process ends. Host code
+// never passes `scratch` itself to a kernel (in host code the name is a
+// stand-in, not a device address): it looks up the array's address on each
+// device once and passes that.
+constexpr size_t kScratchBytes = TC_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
 namespace {
 
-// Argument checks of the backward + update entry point (`what` names the
-// caller in messages).
+// Argument checks shared by the two backward + update entry points (`what`
+// names the caller in messages).
 tc_status check_backward_update(const char *what, const float *grad_out, int32_t num_bags,
                                 int32_t dim, const int32_t *seg_offsets,
                                 const int32_t *casted_src, const int32_t *unique_rows,
@@ -900,6 +908,34 @@ tc_status check_backward_update(const char *what, const float *grad_out, int32_t
     return TC_OK;
 }
 
+// Address of `scratch` on the current device (hipGetSymbolAddress with that
+// device current, looked up once per device), or nullptr with the error set.
+void *scratch_address() {
+    constexpr int kMaxDevices = 64;
+    static void *addr[kMaxDevices] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        set_error("tc_embed_backward_update_noalloc: hipGetDevice: %s", hipGetErrorString(e));
+        return nullptr;
+    }
+    if (dev < 0 || dev >= kMaxDevices) {
+        set_error("tc_embed_backward_update_noalloc: device %d beyond the %d supported", dev,
+                  kMaxDevices);
+        return nullptr;
+    }
+    void *p = __atomic_load_n(&addr[dev], __ATOMIC_ACQUIRE);
+    if (p) return p;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr) {
+        set_error("tc_embed_backward_update_noalloc: hipGetSymbolAddress(scratch): %s",
+                  hipGetErrorString(e));
+        return nullptr;
+    }
+    __atomic_store_n(&addr[dev], p, __ATOMIC_RELEASE);
+    return p;
+}
+
 }  // namespace
 }  // namespace tc
 
@@ -922,6 +958,34 @@ extern "C" tc_status tc_embed_backward_update(
     return launch_backward(grad_out, num_bags, dim, casted_src, seg_offsets, num_unique,
                            max_unique, sink, make_split_ws(workspace, workspace_bytes, dim),
                            stream);
+}
+
+extern "C" tc_status tc_embed_backward_update_noalloc(
+    const float *grad_out, int32_t num_bags, int32_t dim, const int32_t *seg_offsets,
+    const int32_t *casted_src, const int32_t *unique_rows, const int32_t *num_unique,
+    int64_t max_unique, int64_t num_pairs, float *W, float *opt_state, int64_t total_rows,
+    int32_t opt_kind, float lr, float eps, float gamma, float *coal_grad, hipStream_t stream) {
+    clear_error();
+    const tc_status st = check_backward_update(
+        "tc_embed_backward_update_noalloc", grad_out, num_bags, dim, seg_offsets, casted_src,
+        unique_rows, num_unique, max_unique, W, opt_state, total_rows, opt_kind, gamma,
+        coal_grad);
+    if (st != TC_OK) return st;
+    TC_REQUIRE(num_pairs >= 0 && num_pairs < (int64_t(1) << 31), TC_ERR_INVALID_ARG,
+               "tc_embed_backward_update_noalloc: num_pairs must lie in [0, 2^31)");
+    const size_t need = num_pairs < kLongSegment ? 0 : ws_layout(num_pairs, dim).total;
+    TC_REQUIRE(need <= kScratchBytes, TC_ERR_WORKSPACE,
+               "tc_embed_backward_update_noalloc: %lld pairs of dim %d need %zu bytes of "
+               "backward workspace, more than the %zu-byte scratch (TC_NOALLOC_SCRATCH_BYTES); "
+               "use tc_embed_backward_update with a workspace",
+               static_cast<long long>(num_pairs), dim, need, kScratchBytes);
+    if (max_unique == 0) return TC_OK;
+    void *ws = scratch_address();
+    if (ws == nullptr) return TC_ERR_HIP;
+    const RowSink sink{coal_grad, W, opt_state, unique_rows, opt_kind, lr, eps, gamma,
+                       1.0f - gamma};
+    return launch_backward(grad_out, num_bags, dim, casted_src, seg_offsets, num_unique,
+                           max_unique, sink, make_split_ws(ws, kScratchBytes, dim), stream);
 }
 
 extern "C" tc_status tc_embed_expand(const float *grad_out, int32_t num_bags, int32_t dim,

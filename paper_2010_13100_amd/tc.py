@@ -15,6 +15,7 @@ import torch
 from . import build as _build
 
 TC_OK, TC_ERR_INVALID_ARG, TC_ERR_UNSUPPORTED, TC_ERR_WORKSPACE, TC_ERR_HIP = range(5)
+TC_NOALLOC_SCRATCH_BYTES = 16 << 20
 TC_INDEX_OK, TC_INDEX_BAD_TABLE_OFFSETS, TC_INDEX_BAD_BAG_OFFSETS, TC_INDEX_OUT_OF_RANGE = range(4)
 TC_OPT_SGD, TC_OPT_ADAGRAD, TC_OPT_RMSPROP, TC_OPT_ROWWISE_ADAGRAD = range(4)
 OPTIMIZERS = {"sgd": TC_OPT_SGD, "adagrad": TC_OPT_ADAGRAD, "rmsprop": TC_OPT_RMSPROP,
@@ -36,6 +37,9 @@ _SIGNATURES = {
                                 _f32, _vp]),
     "tc_embed_backward_update": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64, _vp, _vp,
                                         _i64, _i32, _f32, _f32, _f32, _vp, _vp, _sz, _vp]),
+    "tc_embed_backward_update_noalloc": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _i64,
+                                                _i64, _vp, _vp, _i64, _i32, _f32, _f32, _f32,
+                                                _vp, _vp]),
     "tc_argsort_rows": (_i32, [_vp, _i32, _i32, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp,
                                _vp, _sz, _vp]),
     "tc_embed_expand": (_i32, [_vp, _i32, _i32, _vp, _i64, _vp, _vp]),
@@ -184,6 +188,19 @@ def tc_embed_backward_update(grad_out, seg_offsets, casted_src, unique_rows, num
         max_unique, _ptr(W, torch.float32, "W"), _ptr(opt_state, torch.float32, "opt_state"),
         W.shape[0], opt_kind, lr, eps, gamma, _ptr(coal_grad, torch.float32, "coal_grad"),
         *_ws(workspace), _stream(stream)), "tc_embed_backward_update")
+
+
+def tc_embed_backward_update_noalloc(grad_out, seg_offsets, casted_src, unique_rows, num_unique,
+                                     max_unique, num_pairs, W, opt_state, opt_kind, lr, eps,
+                                     gamma=0.0, coal_grad=None, stream=None) -> None:
+    _check(_lib.tc_embed_backward_update_noalloc(
+        _ptr(grad_out, torch.float32, "grad_out"), grad_out.shape[0], grad_out.shape[1],
+        _ptr(seg_offsets, torch.int32, "seg_offsets"), _ptr(casted_src, torch.int32, "casted_src"),
+        _ptr(unique_rows, torch.int32, "unique_rows"), _ptr(num_unique, torch.int32, "num_unique"),
+        max_unique, num_pairs, _ptr(W, torch.float32, "W"),
+        _ptr(opt_state, torch.float32, "opt_state"), W.shape[0], opt_kind, lr, eps, gamma,
+        _ptr(coal_grad, torch.float32, "coal_grad"), _stream(stream)),
+        "tc_embed_backward_update_noalloc")
 
 
 def tc_argsort_rows(table_row_offset, num_tables, bags_per_table, total_rows, max_table_rows,

@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(header):
 
 
 def test_version_and_status_strings(tc):
-    assert tc.tc_abi_version() == 6
+    assert tc.tc_abi_version() == 7
     lib = tc._lib
     for code, name in enumerate(["TC_OK", "TC_ERR_INVALID_ARG", "TC_ERR_UNSUPPORTED",
                                  "TC_ERR_WORKSPACE", "TC_ERR_HIP"]):
@@ -227,6 +227,31 @@ def test_backward_and_update_reject_bad_arguments(tc):
     assert coalesce(mu=-3) == tc.TC_ERR_INVALID_ARG
     assert coalesce(sp=None) == tc.TC_ERR_INVALID_ARG
     assert coalesce(mu=0) == tc.TC_OK
+    assert h.untouched()
+
+
+def test_noalloc_backward_update_rejects_bad_arguments(tc):
+    """The no-allocation variant: the checks of tc_embed_backward_update,
+    plus its scratch limit, all before anything is launched or looked up."""
+    lib, h = tc._lib, HostBuffers()
+
+    def f(**k):
+        return lib.tc_embed_backward_update_noalloc(
+            k.get("g", h.fp()), k.get("nb", 10), k.get("dim", 8), k.get("so", h.ip()),
+            k.get("cs", h.ip()), k.get("ur", h.ip()), k.get("nu", h.ip()), k.get("mu", 10),
+            k.get("n", 100), k.get("W", h.fp()), k.get("A", None), k.get("rows", 100),
+            k.get("opt", 0), 0.01, 1e-8, k.get("gamma", 0.9), k.get("coal", None), None)
+    assert f(dim=6) == tc.TC_ERR_UNSUPPORTED and "noalloc" in _err(tc)
+    assert f(opt=3, A=h.fp()) == tc.TC_ERR_UNSUPPORTED
+    assert f(opt=1) == tc.TC_ERR_INVALID_ARG
+    assert f(W=None) == tc.TC_ERR_INVALID_ARG
+    assert f(n=-1) == tc.TC_ERR_INVALID_ARG
+    assert f(n=2 ** 31) == tc.TC_ERR_INVALID_ARG
+    over = 40_000_000
+    assert tc.tc_backward_workspace_bytes(over, 64) > tc.TC_NOALLOC_SCRATCH_BYTES
+    assert f(n=over, dim=64) == tc.TC_ERR_WORKSPACE and "scratch" in _err(tc)
+    assert f(n=over, dim=64, mu=0) == tc.TC_ERR_WORKSPACE
+    assert f(mu=0) == tc.TC_OK and _err(tc) == ""     # nothing to do, nothing looked up
     assert h.untouched()
 
 
