@@ -140,8 +140,8 @@ __device__ __forceinline__ SinkVal sink_value_load(const RowSink &k, int64_t u, 
     SinkVal v{0, 0.f, 0.f};
     if (k.W && col < dim) {
         v.at = int64_t(k.rows[u]) * dim + col;
-        v.w = k.W[v.at];
-        if (k.kind != TC_OPT_SGD) v.a = k.A[v.at];
+        v.w = stream_load(k.W + v.at);
+        if (k.kind != TC_OPT_SGD) v.a = stream_load(k.A + v.at);
     }
     return v;
 }
@@ -160,9 +160,9 @@ __device__ __forceinline__ void sink_value(const RowSink &k, int64_t u, int32_t 
                 adagrad_step(w, a, g, k.lr, k.eps);
             else
                 rmsprop_step(w, a, g, k.lr, k.eps, k.gamma, k.omg);
-            k.A[v.at] = a;
+            stream_store(k.A + v.at, a);
         }
-        k.W[v.at] = w;
+        stream_store(k.W + v.at, w);
     }
 }
 
@@ -180,7 +180,7 @@ __device__ __forceinline__ void sink_group(const RowSink &k, int64_t u, int64_t 
             const int col4 = sub + c * LANES;
             if (col4 >= d4) continue;
             const float4 g = acc[c];
-            float4 w = *reinterpret_cast<const float4 *>(wrow + 4 * col4);
+            float4 w = stream_load4(wrow + 4 * col4);
             if (k.kind == TC_OPT_SGD) {
                 w.x = sgd_step(w.x, g.x, k.lr);
                 w.y = sgd_step(w.y, g.y, k.lr);
@@ -188,7 +188,7 @@ __device__ __forceinline__ void sink_group(const RowSink &k, int64_t u, int64_t 
                 w.w = sgd_step(w.w, g.w, k.lr);
             } else {
                 float *arow = k.A + r * dim;
-                float4 a = *reinterpret_cast<const float4 *>(arow + 4 * col4);
+                float4 a = stream_load4(arow + 4 * col4);
                 if (k.kind == TC_OPT_ADAGRAD) {
                     adagrad_step(w.x, a.x, g.x, k.lr, k.eps);
                     adagrad_step(w.y, a.y, g.y, k.lr, k.eps);
@@ -200,9 +200,9 @@ __device__ __forceinline__ void sink_group(const RowSink &k, int64_t u, int64_t 
                     rmsprop_step(w.z, a.z, g.z, k.lr, k.eps, k.gamma, k.omg);
                     rmsprop_step(w.w, a.w, g.w, k.lr, k.eps, k.gamma, k.omg);
                 }
-                *reinterpret_cast<float4 *>(arow + 4 * col4) = a;
+                stream_store4(arow + 4 * col4, a);
             }
-            *reinterpret_cast<float4 *>(wrow + 4 * col4) = w;
+            stream_store4(wrow + 4 * col4, w);
         }
     }
 }

@@ -74,12 +74,12 @@ __global__ __launch_bounds__(kBlock) void k_sparse_update(
             for (int c = 0; c < CHUNKS; ++c) {
                 const int col4 = sub + c * LANES;
                 if (col4 >= d4) continue;
-                float4 w = *reinterpret_cast<const float4 *>(wrow + 4 * col4);
+                float4 w = stream_load4(wrow + 4 * col4);
                 w.x = w.x - lr * (g[c].x / s);
                 w.y = w.y - lr * (g[c].y / s);
                 w.z = w.z - lr * (g[c].z / s);
                 w.w = w.w - lr * (g[c].w / s);
-                *reinterpret_cast<float4 *>(wrow + 4 * col4) = w;
+                stream_store4(wrow + 4 * col4, w);
             }
             // this row's reads of the group's LDS slice are issued before the
             // next row's stores to it (program order within the wave)
@@ -91,7 +91,7 @@ __global__ __launch_bounds__(kBlock) void k_sparse_update(
             const int col4 = sub + c * LANES;
             if (col4 >= d4) continue;
             const float4 g = *reinterpret_cast<const float4 *>(grow + 4 * col4);
-            float4 w = *reinterpret_cast<const float4 *>(wrow + 4 * col4);
+            float4 w = stream_load4(wrow + 4 * col4);
             if constexpr (OPT == TC_OPT_SGD) {
                 w.x = sgd_step(w.x, g.x, lr);
                 w.y = sgd_step(w.y, g.y, lr);
@@ -99,7 +99,7 @@ __global__ __launch_bounds__(kBlock) void k_sparse_update(
                 w.w = sgd_step(w.w, g.w, lr);
             } else {
                 float *arow = A + r * int64_t(dim);
-                float4 a = *reinterpret_cast<const float4 *>(arow + 4 * col4);
+                float4 a = stream_load4(arow + 4 * col4);
                 if constexpr (OPT == TC_OPT_ADAGRAD) {
                     adagrad_step(w.x, a.x, g.x, lr, eps);
                     adagrad_step(w.y, a.y, g.y, lr, eps);
@@ -111,9 +111,9 @@ __global__ __launch_bounds__(kBlock) void k_sparse_update(
                     rmsprop_step(w.z, a.z, g.z, lr, eps, gamma, omg);
                     rmsprop_step(w.w, a.w, g.w, lr, eps, gamma, omg);
                 }
-                *reinterpret_cast<float4 *>(arow + 4 * col4) = a;
+                stream_store4(arow + 4 * col4, a);
             }
-            *reinterpret_cast<float4 *>(wrow + 4 * col4) = w;
+            stream_store4(wrow + 4 * col4, w);
         }
     }
 }
