@@ -25,23 +25,39 @@ _CFLAGS = ["-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fas
            "-Wall", "-Wextra"]
 
 
-def lib_path(precision: str) -> str:
-    return os.path.join(_HERE, f"liboracle_{precision}.so")
+# The sanitized builds (TC_SANITIZED=1 in the environment selects them) use
+# clang's AddressSanitizer and UndefinedBehaviorSanitizer; the process
+# preloads clang's sanitizer runtime (tests/test_sanitizers.py).
+_SAN_CC = "/opt/rocm/llvm/bin/clang"
+_SAN_FLAGS = ["-g", "-O1", "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+              "-fno-omit-frame-pointer"]
 
 
-def build_one(src: str, precision: str, out: str, verbose: bool = False) -> None:
-    """Compile one oracle source for ``precision`` ("f64" or "f32") with gcc."""
+def sanitized() -> bool:
+    return os.environ.get("TC_SANITIZED") == "1"
+
+
+def lib_path(precision: str, san: bool | None = None) -> str:
+    san = sanitized() if san is None else san
+    return os.path.join(_HERE, f"liboracle_{precision}{'_san' if san else ''}.so")
+
+
+def build_one(src: str, precision: str, out: str, verbose: bool = False,
+              san: bool = False) -> None:
+    """Compile one oracle source for ``precision`` ("f64" or "f32") with gcc
+    (or, san=True, with clang and the sanitizers)."""
     ctype = {"f64": "double", "f32": "float"}[precision]
-    cmd = ["gcc", *_CFLAGS, f"-DOREAL={ctype}", src, "-o", out, "-lm"]
+    cc, extra = (_SAN_CC, _SAN_FLAGS) if san else ("gcc", [])
+    cmd = [cc, *_CFLAGS, *extra, f"-DOREAL={ctype}", src, "-o", out, "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)
 
 
-def build(verbose: bool = False) -> None:
+def build(verbose: bool = False, san: bool = False) -> None:
     """Compile the f64 and f32 oracle libraries."""
     for prec in ("f64", "f32"):
-        build_one(_SRC, prec, lib_path(prec), verbose)
+        build_one(_SRC, prec, lib_path(prec, san), verbose, san)
 
 
 _i32p = ctypes.POINTER(ctypes.c_int32)
@@ -72,7 +88,7 @@ class Oracle:
         if path is None:
             path = lib_path(precision)
             if not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_SRC):
-                build()
+                build(san=sanitized())
         lib = ctypes.CDLL(path)
         self.precision = precision
         self.dtype = np.float64 if precision == "f64" else np.float32

@@ -1,5 +1,6 @@
 // Status codes, per-thread error messages and launch checks of libtc.
 #include <cstdarg>
+#include <cstring>
 
 #include "tc_internal.h"
 
@@ -44,7 +45,11 @@ tc_status check_launch(const char *what) {
 }  // namespace tc
 
 extern "C" const char *tc_status_string(tc_status status) {
-    switch (status) {
+    // callers may pass any int; read it as one (an enum load of a value
+    // outside the enumerators' range would be undefined in C++)
+    int32_t code = 0;
+    std::memcpy(&code, &status, sizeof(code));
+    switch (code) {
         case TC_OK: return "TC_OK";
         case TC_ERR_INVALID_ARG: return "TC_ERR_INVALID_ARG";
         case TC_ERR_UNSUPPORTED: return "TC_ERR_UNSUPPORTED";

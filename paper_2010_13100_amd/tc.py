@@ -58,7 +58,11 @@ class TcError(RuntimeError):
 
 
 def load_library(path: str | None = None) -> ctypes.CDLL:
-    path = path or _build.lib_path("libtc.so")
+    """libtc.so, or with TC_SANITIZED=1 in the environment the build with the
+    host code under AddressSanitizer and UBSan (libtc_san.so; the process
+    must preload the sanitizer runtime)."""
+    san = os.environ.get("TC_SANITIZED") == "1"
+    path = path or _build.lib_path("libtc_san.so" if san else "libtc.so")
     if not os.path.exists(path):
         raise ImportError(f"libtc not built: {path} is missing (run __graft_entry__.build())")
     lib = ctypes.CDLL(path)
