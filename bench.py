@@ -247,18 +247,14 @@ def write_traffic(pmc_dir: str, workload: str, calls) -> dict:
     return table
 
 
-def cpu_baseline(w, batch, budget_s: float):
-    """The fp32 oracle (single thread) on a bounded sample of the workload:
-    forward, casting, the baseline expand + coalesce backward and the update,
-    on the rows the sample touches. The sample is the first whole tables (or,
-    for one table, the first bags) holding about 84M gathered floats (a
-    1.3M-pair batch of 64-float rows, about half a second of oracle work);
-    steps/s is scaled to the full batch by its share of the pairs."""
+def cpu_sample(w, batch):
+    """A bounded sample of batch 0 for the CPU baselines: the first whole
+    tables (or, for one table, the first bags) holding about 84M gathered
+    floats (a 1.3M-pair batch of 64-float rows, about half a second of
+    single-threaded oracle work)."""
     import numpy as np
 
-    import oracle
     from paper_2010_13100_amd import workload as wl
-    orc = oracle.Oracle("f32")
     target_pairs = max(1, 84_000_000 // w.dim)
     bo = batch.bag_offsets
     if batch.num_pairs <= target_pairs:
@@ -275,28 +271,79 @@ def cpu_baseline(w, batch, budget_s: float):
     n = int(s_bo[-1])
     s_idx = batch.indices[:n]
     s_off = batch.table_row_offset[:tables + 1].copy()
-    s_grad = batch.grad_out[:nb]
     t = np.repeat(np.arange(nb) // bags, np.diff(s_bo))
-    ids = np.unique(s_off[t] + s_idx)
-    table = wl.table_rows(w, ids)
+    src = s_off[t] + s_idx
+    ids = np.unique(src)
+    return dict(tables=tables, bags=bags, bo=s_bo, idx=s_idx, off=s_off, grad=batch.grad_out[:nb],
+                n=n, ids=ids, pair_row=np.searchsorted(ids, src).astype(np.int32),
+                table=wl.table_rows(w, ids),
+                text=f"the first {tables} table(s) x {bags} bags of batch 0: {n} of "
+                     f"{batch.num_pairs} pairs, {len(ids)} table rows")
+
+
+def cpu_baseline(w, batch, budget_s: float, sample=None):
+    """The fp32 oracle (single thread) on a bounded sample of the workload
+    (cpu_sample): forward, casting, the baseline expand + coalesce backward
+    and the update, on the rows the sample touches; steps/s is scaled to the
+    full batch by the sample's share of the pairs."""
+    import numpy as np
+
+    import oracle
+    orc = oracle.Oracle("f32")
+    s = sample or cpu_sample(w, batch)
     steps, t0 = 0, time.perf_counter()
     phases: dict = {}
     while True:
-        oracle.train_step(orc, num_tables=tables, bags_per_table=bags, table_row_offset=s_off,
-                          indices=s_idx, bag_offsets=s_bo, grad_out=s_grad, table=table,
-                          table_ids=ids, optimizer=w.optimizer, lr=np.float32(w.lr),
-                          eps=np.float32(w.eps), gamma=np.float32(w.gamma), timings=phases)
+        oracle.train_step(orc, num_tables=s["tables"], bags_per_table=s["bags"],
+                          table_row_offset=s["off"], indices=s["idx"], bag_offsets=s["bo"],
+                          grad_out=s["grad"], table=s["table"], table_ids=s["ids"],
+                          optimizer=w.optimizer, lr=np.float32(w.lr), eps=np.float32(w.eps),
+                          gamma=np.float32(w.gamma), timings=phases)
         steps += 1
         el = time.perf_counter() - t0
         if el >= budget_s or steps >= 50:
             break
-    share = n / batch.num_pairs
+    share = s["n"] / batch.num_pairs
     return {"value": steps / el * share, "unit": "steps/s", "cores": 1, "kind": "oracle",
-            "sample": f"{steps} oracle steps (fp32, one thread) on the first {tables} "
-                      f"table(s) x {bags} bags of batch 0: {n} of {batch.num_pairs} pairs, "
-                      f"{len(ids)} table rows; steps/s scaled by that share of the pairs",
+            "sample": f"{steps} oracle steps (fp32, one thread) on {s['text']}; steps/s "
+                      "scaled by that share of the pairs",
             "sample_steps_per_s": round(steps / el, 4),
             "seconds_per_phase": {k: round(v / steps, 4) for k, v in phases.items()}}
+
+
+def cpu_baseline_allcores(w, batch, budget_s: float, sample=None):
+    """The paper's baseline step (forward, expand, stable argsort,
+    Algorithm 1, update) on all host cores with OpenMP (cpu_baseline/, equal
+    to the oracle bit for bit), on the same sample as cpu_baseline."""
+    import numpy as np
+
+    import cpu_baseline as cb_mod
+    if w.optimizer not in ("sgd", "adagrad"):
+        return None
+    cb = cb_mod.CpuBaseline()
+    s = sample or cpu_sample(w, batch)
+    steps, t0 = 0, time.perf_counter()
+    phases: dict = {}
+    while True:
+        table = s["table"].copy()
+        acc = np.zeros_like(table) if w.optimizer == "adagrad" else None
+        t1 = time.perf_counter()
+        _, _, _, ph = cb.train_step(s["bo"], s["pair_row"], table, s["grad"], w.optimizer, acc,
+                                    np.float32(w.lr), np.float32(w.eps))
+        for k, v in ph.items():
+            phases[k] = phases.get(k, 0.0) + v
+        steps += 1
+        phases["_step"] = phases.get("_step", 0.0) + time.perf_counter() - t1
+        if time.perf_counter() - t0 >= budget_s or steps >= 200:
+            break
+    step_s = phases.pop("_step") / steps
+    share = s["n"] / batch.num_pairs
+    return {"value": 1.0 / step_s * share, "unit": "steps/s", "cores": cb.threads,
+            "kind": "openmp expand-coalesce (the paper's baseline step, all host cores)",
+            "sample": f"{steps} steps on {s['text']} (table copy per step not timed); "
+                      "steps/s scaled by that share of the pairs",
+            "sample_steps_per_s": round(1.0 / step_s, 4),
+            "seconds_per_phase": {k: round(v / steps, 5) for k, v in phases.items()}}
 
 
 def setup(w, dev):
@@ -636,7 +683,11 @@ def main():
     result["host"] = host_cpu()
     if args.cpu_budget > 0:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(w, batch0, args.cpu_budget)
+        sample = cpu_sample(w, batch0)
+        result["cpu_baseline"] = cpu_baseline(w, batch0, args.cpu_budget, sample)
+        print("[bench] timing the all-cores CPU baseline", file=sys.stderr, flush=True)
+        result["cpu_baseline_allcores"] = cpu_baseline_allcores(w, batch0, args.cpu_budget / 2,
+                                                                sample)
     else:
         result["cpu_baseline"] = None
     print(json.dumps(result), flush=True)
