@@ -593,6 +593,46 @@ def run_workload(args, cfg_name, dev, keep_batch=False):
     return res, keep, w
 
 
+def run_forward_span(args, w, dev, spans):
+    """The forward gather-reduce alone on the workload's shape with each
+    table's row ids drawn uniformly from its first R rows, for each R in
+    spans: how the gather rate depends on the address range the random
+    row reads cover (translation reach, caches). One JSON line per span."""
+    import numpy as np
+    import torch
+
+    from paper_2010_13100_amd import device_fill, tc
+
+    T, B, D = w.num_tables, w.batch, w.dim
+    W = torch.empty((w.total_rows, D), dtype=torch.float32, device=dev)
+    device_fill.fill_uniform(W, seed=0, lo=w.init_lo, hi=w.init_hi)
+    lengths = np.full(T * B, w.pooling_value, np.int64)
+    bo = torch.from_numpy(np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)).to(dev)
+    off = torch.from_numpy(np.arange(T + 1, dtype=np.int64) * w.rows_per_table).to(dev)
+    out = torch.empty((T * B, D), dtype=torch.float32, device=dev)
+    rng = np.random.default_rng(0)
+    n = int(lengths.sum())
+    for span in spans:
+        span = min(span, w.rows_per_table)
+        idx = torch.from_numpy(rng.integers(0, span, size=n).astype(np.int32)).to(dev)
+        for _ in range(args.warmup):
+            tc.tc_embed_forward(W, off, T, B, idx, bo, out)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            tc.tc_embed_forward(W, off, T, B, idx, bo, out)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / args.steps
+        nbytes = n * (4 + 4 * D) + (T * B + 1) * 4 + T * B * 4 * D
+        print(json.dumps({"forward_span_rows": span, "span_MB_per_table": span * D * 4 / 1e6,
+                          "workload": w.name, "us": round(us, 1),
+                          "algorithmic_GBps": round(nbytes / us / 1e3, 1),
+                          "frac_of_hbm_peak": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4)}),
+              flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -623,6 +663,9 @@ def main():
     ap.add_argument("--sweep", default=None, metavar="batch=B1,B2,..|dim=D1,D2,..",
                     help="sensitivity sweep: step and backward A/B per value, one JSON line "
                          "each, then exit")
+    ap.add_argument("--forward-span", default=None, metavar="R1,R2,..",
+                    help="time the forward alone on --config's shape with each table's rows "
+                         "drawn from its first R rows, per R, one JSON line each, then exit")
     ap.add_argument("--profile-steps", action="store_true",
                     help="for profiler runs: run warmup + steps steps of --config and "
                          "nothing else on the GPU (no events, no extra casts), print one "
@@ -657,6 +700,10 @@ def main():
     from paper_2010_13100_amd import workload as wl
 
     dev = torch.device("cuda", 0)
+    if args.forward_span:
+        run_forward_span(args, wl.WORKLOADS[args.config], dev,
+                         [int(x) for x in args.forward_span.split(",")])
+        return
     if args.sweep or args.ab or args.profile_steps:
         w = wl.variant(wl.WORKLOADS[args.config], batch=args.batch, dim=args.dim,
                        optimizer=args.optimizer)
