@@ -345,10 +345,11 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool ok) {
 }
 
 // The same with the digit width known only at run time (uniform branches).
+template <int MAXB = kMaxRadixBits>
 __device__ __forceinline__ uint64_t match_digit_n(uint32_t d, bool ok, int bits) {
     uint64_t peers = __ballot(ok);
 #pragma unroll
-    for (int b = 0; b < kMaxRadixBits; ++b) {
+    for (int b = 0; b < MAXB; ++b) {
         if (b < bits) {
             const bool bit = (d >> b) & 1u;
             const uint64_t m = __ballot(bit);
@@ -673,6 +674,12 @@ constexpr int kSmallWaves = kSmallThreads / kWave;  // 16
 constexpr int kSmallItems = 8;
 constexpr int kSmallSpan = kWave * kSmallItems;     // 512
 constexpr int kSmallPairs = kSmallWaves * kSmallSpan;  // 8192
+// Digits of up to 9 bits in the one-workgroup cast: its per-wave digit
+// counts stay in LDS (16 x 512), and 17- or 18-bit keys take two passes
+// instead of three.
+constexpr int kSmallRadixBits = 9;
+constexpr int kSmallRadix = 1 << kSmallRadixBits;
+static_assert(kSmallRadix <= kSmallThreads, "one digit per thread in the digit scan");
 static_assert(kSmallPairs == kSmallItems * kSmallThreads, "k_cast_small stages one item per trip");
 
 // Block-wide exclusive scan over the kSmallThreads threads.
@@ -710,9 +717,11 @@ __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
     int32_t bags_per_table, int32_t n, int bits, bool positions, int32_t *__restrict__ unique_rows,
     int32_t *__restrict__ seg_offsets, int32_t *__restrict__ casted_src,
     int32_t *__restrict__ casted_dst, int32_t *__restrict__ num_unique, FwdSlice fs) {
+    // keys ping-pong between two buffers; values have one: every item of a
+    // pass is in registers before the pass writes any (barriers between)
     __shared__ int32_t keys[2][kSmallPairs];
-    __shared__ int32_t vals[2][kSmallPairs];
-    __shared__ int32_t wcount[kSmallWaves][kMaxRadix];
+    __shared__ int32_t vals[kSmallPairs];
+    __shared__ int32_t wcount[kSmallWaves][kSmallRadix];
     if constexpr (FL > 0) {
         if (blockIdx.x > 0) {  // uniform: a forward workgroup
             constexpr int64_t kWaves = kSmallThreads / kWave;
@@ -725,13 +734,15 @@ __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
 
     // (src, dst) pairs from the bag-major CSR index: 16 lanes per bag. The
     // index, the bag offsets and the table offsets are first staged in LDS
-    // (in the second key and value buffers and the digit counters) with
-    // independent loads, so the walk over bags waits for memory once.
+    // (in the value buffer, the second key buffer and the digit counters)
+    // with independent loads, so the walk over bags waits for memory once.
+    // The index shares the value buffer: position j's index is read and its
+    // value then written by the same thread, and no other.
     {
         constexpr int kLanes = 16;
         const int sub = tid & (kLanes - 1);
-        const bool staged = num_bags < kSmallPairs && num_tables <= kSmallWaves * kMaxRadix;
-        int32_t *s_idx = keys[1], *s_bo = vals[1], *s_off = &wcount[0][0];
+        const bool staged = num_bags < kSmallPairs && num_tables <= kSmallWaves * kSmallRadix;
+        int32_t *s_idx = vals, *s_bo = keys[1], *s_off = &wcount[0][0];
         if (staged) {
             // every load issued before the first LDS store (n and num_bags
             // + 1 are at most kSmallPairs = kSmallItems * kSmallThreads), so
@@ -760,13 +771,13 @@ __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
             const int32_t base = staged ? s_off[t] : int32_t(table_row_offset[t]);
             for (int32_t j = beg + sub; j < end; j += kLanes) {
                 keys[0][j] = base + (staged ? s_idx[j] : indices[j]);
-                vals[0][j] = positions ? j : g;
+                vals[j] = positions ? j : g;
             }
         }
     }
     __syncthreads();
 
-    const int passes = (bits + kMaxRadixBits - 1) / kMaxRadixBits;
+    const int passes = (bits + kSmallRadixBits - 1) / kSmallRadixBits;
     const int per_pass = (bits + passes - 1) / passes;
     // trips of 64 positions per wavefront (at most kSmallItems), so that
     // every wavefront holds a share of the pairs
@@ -777,7 +788,7 @@ __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
         const int shift = p * per_pass;
         const int pbits = shift + per_pass <= bits ? per_pass : bits - shift;
         const uint32_t mask = (1u << pbits) - 1u;
-        for (int i = tid; i < kSmallWaves * kMaxRadix; i += kSmallThreads)
+        for (int i = tid; i < kSmallWaves * kSmallRadix; i += kSmallThreads)
             (&wcount[0][0])[i] = 0;
         __syncthreads();
         int32_t key[kSmallItems], val[kSmallItems], lower_n[kSmallItems], leader[kSmallItems],
@@ -791,11 +802,11 @@ __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
             const int32_t j = base + i * kWave + lane;
             const bool ok = j < n;
             key[i] = ok ? keys[cur][j] : 0;
-            val[i] = ok ? vals[cur][j] : 0;
+            val[i] = ok ? vals[j] : 0;
             const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
             uint64_t act;
             const uint64_t peers =
-                all_same_digit(d, ok, &act) ? act : match_digit_n(d, ok, pbits);
+                all_same_digit(d, ok, &act) ? act : match_digit_n<kSmallRadixBits>(d, ok, pbits);
             const uint64_t lower = peers & lanemask_lt(lane);
             lower_n[i] = __popcll(lower);
             leader[i] = peers ? __builtin_ctzll(peers) : lane;
@@ -813,12 +824,12 @@ __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
             int32_t c[kSmallWaves], my = 0;
 #pragma unroll
             for (int ww = 0; ww < kSmallWaves; ++ww) {
-                c[ww] = tid < kMaxRadix ? wcount[ww][tid] : 0;
+                c[ww] = tid < kSmallRadix ? wcount[ww][tid] : 0;
                 my += c[ww];
             }
             int32_t tot;
             int32_t r = small_block_scan(my, &tot);
-            if (tid < kMaxRadix) {
+            if (tid < kSmallRadix) {
 #pragma unroll
                 for (int ww = 0; ww < kSmallWaves; ++ww) {
                     wcount[ww][tid] = r;
@@ -833,7 +844,7 @@ __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
                 const uint32_t d = (uint32_t(key[i]) >> shift) & mask;
                 const int32_t lp = wcount[w][d] + rank[i];
                 keys[cur ^ 1][lp] = key[i];
-                vals[cur ^ 1][lp] = val[i];
+                vals[lp] = val[i];
             }
         }
         __syncthreads();
@@ -856,7 +867,7 @@ __global__ __launch_bounds__(kSmallThreads) void k_cast_small(
         const int32_t j = tid * trips + i;
         if (i < trips && j < n) {
             run += head[i];
-            casted_src[j] = vals[cur][j];
+            casted_src[j] = vals[j];
             if (casted_dst) casted_dst[j] = run - 1;
             if (head[i]) {
                 unique_rows[run - 1] = keys[cur][j];
