@@ -96,7 +96,7 @@ KERNEL_NAMES = {
     "update": ["k_sparse_update"],
     "cast": ["k_cast_small", "k_build_keys", "k_radix_hist", "k_radix_scan", "k_radix_scatter",
              "k_seg_count", "k_seg_write"],
-    # the forward's bags run inside the scatters (or beside k_cast_small)
+    # the forward's bags run in the pair build's launch (or beside k_cast_small)
     "forward_cast": ["k_cast_small", "k_forward_build", "k_radix_hist", "k_radix_scan",
                      "k_radix_scatter", "k_seg_count", "k_seg_write", "k_forward"],
 }
