@@ -55,7 +55,7 @@ def to_dev(a: np.ndarray) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-class GpuRun:
+class DeviceRun:
     """A trainer plus device copies of its batches."""
 
     def __init__(self, w: wl.Workload, max_pairs: int, fill_on_device=True, table=None,
@@ -245,7 +245,7 @@ def check_step_against_definition(cast: dict, split, out, out64, coal, coal64,
     return np.asarray(cast["unique_rows"], np.int64)[long_chain]
 
 
-def check_against_definition(run: "GpuRun", model64: "OracleModel", shadow64: "OracleModel",
+def check_against_definition(run: "DeviceRun", model64: "OracleModel", shadow64: "OracleModel",
                              what: str, exclude=()):
     """The GPU's updated table and accumulator rows against the fp64
     definition, after the same steps, within the 1e-5 row-normwise tolerance:

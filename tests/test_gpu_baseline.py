@@ -8,7 +8,7 @@ import torch
 
 import oracle
 from paper_2010_13100_amd import workload as wl
-from tests.gpu_harness import GpuRun, assert_close, to_dev
+from tests.gpu_harness import DeviceRun, assert_close, to_dev
 from tests.test_gpu_parity import SMALL
 
 pytestmark = pytest.mark.gpu
@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 def run_both(w, b):
     """Casted backward, then the baseline on the same trainer; returns both
     results and the oracle's."""
-    run = GpuRun(w, max_pairs=max(b.num_pairs, 1))
+    run = DeviceRun(w, max_pairs=max(b.num_pairs, 1))
     t = run.trainer
     off, idx, bo, g = (to_dev(b.table_row_offset), to_dev(b.indices), to_dev(b.bag_offsets),
                        to_dev(b.grad_out))

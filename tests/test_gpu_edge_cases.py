@@ -5,7 +5,7 @@ import numpy as np
 import pytest
 
 from paper_2010_13100_amd import workload as wl
-from tests.gpu_harness import GpuRun, OracleModel, assert_close, compare_cast
+from tests.gpu_harness import DeviceRun, OracleModel, assert_close, compare_cast
 
 pytestmark = pytest.mark.gpu
 
@@ -37,7 +37,7 @@ def check(w, b):
 
 def check_one(w, b, fused):
     print(f"\n[{w.name} fused={fused}] pairs {b.num_pairs}", flush=True)
-    run = GpuRun(w, max_pairs=max(b.num_pairs, 1))
+    run = DeviceRun(w, max_pairs=max(b.num_pairs, 1))
     t = np.repeat(np.arange(w.num_bags) // w.batch, np.diff(b.bag_offsets))
     touched = np.unique(b.table_row_offset[t] + b.indices)
     model = OracleModel(w, touched if len(touched) else np.zeros(1, np.int64))

@@ -18,7 +18,7 @@ import torch
 
 import oracle
 from paper_2010_13100_amd import workload as wl
-from tests.gpu_harness import (FP32_CHAIN_LIMIT, SPLIT_PAIRS, GpuRun, assert_close,
+from tests.gpu_harness import (FP32_CHAIN_LIMIT, SPLIT_PAIRS, DeviceRun, assert_close,
                                check_step_slope, compare_cast, piecewise_row, scatter, step_slope)
 
 pytestmark = pytest.mark.gpu
@@ -39,7 +39,7 @@ def test_full_size_step(cfg, split, opt, stored):
     w = wl.variant(wl.WORKLOADS[cfg], optimizer=opt)
     b = wl.make_batch(w, step=0)
     print(f"\n[{cfg} split={split} stored={stored}] {w.name}: {b.num_pairs} pairs", flush=True)
-    run = GpuRun(w, max_pairs=b.num_pairs, split_long=split)
+    run = DeviceRun(w, max_pairs=b.num_pairs, split_long=split)
     assert run.split_cap >= b.num_pairs if split else run.split_cap == 0
     run.run_step(b, with_casted_dst=stored, fused=True, store_coal=stored)
     t = run.trainer

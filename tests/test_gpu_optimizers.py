@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 
 from paper_2010_13100_amd import workload as wl
-from tests.gpu_harness import (GpuRun, OracleModel, assert_close, check_against_definition,
+from tests.gpu_harness import (DeviceRun, OracleModel, assert_close, check_against_definition,
                                check_step_against_definition)
 
 pytestmark = pytest.mark.gpu
@@ -28,7 +28,7 @@ def run_steps(w, fused, steps=3):
     touched = np.unique(np.concatenate([global_rows(w, b) for b in batches]))
     print(f"\n[{w.name} {w.optimizer} gamma={w.gamma} fused={fused}] pairs "
           f"{[b.num_pairs for b in batches]} touched {len(touched)}", flush=True)
-    run = GpuRun(w, max_pairs=max(b.num_pairs for b in batches))
+    run = DeviceRun(w, max_pairs=max(b.num_pairs for b in batches))
     model = OracleModel(w, touched)
     model64 = OracleModel(w, touched, precision="f64")
     shadow64 = OracleModel(w, touched, precision="f64")

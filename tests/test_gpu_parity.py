@@ -14,7 +14,7 @@ import pytest
 import torch
 
 from paper_2010_13100_amd import workload as wl
-from tests.gpu_harness import (GpuRun, OracleModel, assert_close, check_against_definition,
+from tests.gpu_harness import (DeviceRun, OracleModel, assert_close, check_against_definition,
                                check_step_against_definition, compare_cast)
 
 pytestmark = pytest.mark.gpu
@@ -49,7 +49,7 @@ def test_two_steps_match_oracle(name, bound, fused):
     touched = np.unique(np.concatenate([global_rows(w, b) for b in batches]))
     print(f"\n[{name} {bound} fused={fused}] pairs {[b.num_pairs for b in batches]} "
           f"touched {len(touched)}", flush=True)
-    run = GpuRun(w, max_pairs=max(b.num_pairs for b in batches),
+    run = DeviceRun(w, max_pairs=max(b.num_pairs for b in batches),
                  max_table_rows=None if bound == "table-local" else 0)
     model = OracleModel(w, touched)
     model64 = OracleModel(w, touched, precision="f64")
@@ -81,7 +81,7 @@ def test_deterministic_across_runs():
     b = wl.make_batch(w, 3)
     res = []
     for _ in range(2):
-        run = GpuRun(w, max_pairs=b.num_pairs)
+        run = DeviceRun(w, max_pairs=b.num_pairs)
         out, cast, coal = run.step(b)
         res.append((out, cast["casted_src"], coal, run.trainer.W.cpu().numpy()))
         run.release()

@@ -19,7 +19,7 @@ import torch
 import oracle
 from paper_2010_13100_amd import tc
 from paper_2010_13100_amd import workload as wl
-from tests.gpu_harness import (GpuRun, OracleModel, assert_close, check_against_definition,
+from tests.gpu_harness import (DeviceRun, OracleModel, assert_close, check_against_definition,
                                check_step_against_definition, compare_cast, is_split, to_dev)
 
 pytestmark = pytest.mark.gpu
@@ -42,7 +42,7 @@ def global_rows(w, b):
 def run_steps(w, batches, fused, run=None, cap=None):
     touched = np.unique(np.concatenate([global_rows(w, b) for b in batches]))
     if run is None:
-        run = GpuRun(w, max_pairs=max(b.num_pairs for b in batches), split_long=True)
+        run = DeviceRun(w, max_pairs=max(b.num_pairs for b in batches), split_long=True)
     model = OracleModel(w, touched, split_cap=run.split_cap if cap is None else cap)
     model64 = OracleModel(w, touched, precision="f64")
     shadow64 = OracleModel(w, touched, precision="f64")
@@ -128,7 +128,7 @@ def test_stale_and_garbage_workspace():
     split segments sit elsewhere: entries of other calls are never taken."""
     w = SHAPES["c2-2x20k"]
     b0, b1 = wl.make_batch(w, 0), wl.make_batch(w, 5)
-    run = GpuRun(w, max_pairs=max(b0.num_pairs, b1.num_pairs), split_long=True)
+    run = DeviceRun(w, max_pairs=max(b0.num_pairs, b1.num_pairs), split_long=True)
     ws = run.trainer.bwd_workspace
     gen = torch.Generator(device="cuda").manual_seed(3)
     ws.view(torch.int32)[:] = torch.randint(-5, 2000, (ws.numel() // 4,), generator=gen,
@@ -142,7 +142,7 @@ def test_workspace_covering_part_of_the_batch():
     sorted order) is split, the late one is summed as one chain."""
     w, b = hot_batch([9000, 9000], 64, rows=1000, filler=22_000, seed=7, hot_rows=[3, 996])
     half = b.num_pairs // 2
-    run = GpuRun(w, max_pairs=b.num_pairs, split_long=True)
+    run = DeviceRun(w, max_pairs=b.num_pairs, split_long=True)
     small = tc.tc_backward_workspace_bytes(half, w.dim)
     run.trainer.bwd_workspace = torch.empty(small, dtype=torch.uint8, device="cuda")
     # the cover is at least `half` pairs and, from the layout, less than
@@ -156,7 +156,7 @@ def test_workspace_covering_part_of_the_batch():
 
 def test_no_workspace_is_one_chain():
     w, b = hot_batch([9000], 64, seed=9)
-    run = GpuRun(w, max_pairs=b.num_pairs, split_long=False)
+    run = DeviceRun(w, max_pairs=b.num_pairs, split_long=False)
     assert run.trainer.bwd_workspace is None
     _, nsplit = run_steps(w, [b], True, run=run)
     assert nsplit == 0
@@ -168,7 +168,7 @@ def test_repeats_bit_for_bit():
     b = wl.make_batch(w, 2)
     res = []
     for _ in range(2):
-        run = GpuRun(w, max_pairs=b.num_pairs, split_long=True)
+        run = DeviceRun(w, max_pairs=b.num_pairs, split_long=True)
         out, cast, coal = run.step(b, fused=True)
         res.append((coal, run.trainer.W.cpu().numpy()))
         run.release()
@@ -178,7 +178,7 @@ def test_repeats_bit_for_bit():
 def test_baseline_coalesce_pieces_equal_casted():
     w = SHAPES["c2-2x20k"]
     b = wl.make_batch(w, 0)
-    run = GpuRun(w, max_pairs=b.num_pairs, split_long=True)
+    run = DeviceRun(w, max_pairs=b.num_pairs, split_long=True)
     t = run.trainer
     off, idx, bo, g = (to_dev(b.table_row_offset), to_dev(b.indices), to_dev(b.bag_offsets),
                        to_dev(b.grad_out))

@@ -12,7 +12,7 @@ import torch
 
 from paper_2010_13100_amd import tc
 from paper_2010_13100_amd import workload as wl
-from tests.gpu_harness import GpuRun, assert_close, to_dev
+from tests.gpu_harness import DeviceRun, assert_close, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -33,8 +33,8 @@ def test_noalloc_matches_workspace_call_twice():
         b = wl.make_batch(w, step)
         print(f"\n[noalloc] {w.name}: {b.num_pairs} pairs", flush=True)
         assert tc.tc_backward_workspace_bytes(b.num_pairs, w.dim) <= tc.TC_NOALLOC_SCRATCH_BYTES
-        ref = GpuRun(w, max_pairs=b.num_pairs, split_long=True)
-        got = GpuRun(w, max_pairs=b.num_pairs, split_long=False)
+        ref = DeviceRun(w, max_pairs=b.num_pairs, split_long=True)
+        got = DeviceRun(w, max_pairs=b.num_pairs, split_long=False)
         for r in (ref, got):
             g = cast_and_grad(r, b)
         t_ref, t_got = ref.trainer, got.trainer
@@ -69,8 +69,8 @@ def test_noalloc_row_shapes_and_optimizers(dim, opt):
     w = W["c2"].scaled(name=f"noalloc-d{dim}", num_tables=2, rows_per_table=5_000, dim=dim,
                        batch=300, optimizer=opt)
     b = wl.make_batch(w, 0)
-    ref = GpuRun(w, max_pairs=b.num_pairs, split_long=True)
-    got = GpuRun(w, max_pairs=b.num_pairs, split_long=False)
+    ref = DeviceRun(w, max_pairs=b.num_pairs, split_long=True)
+    got = DeviceRun(w, max_pairs=b.num_pairs, split_long=False)
     for r in (ref, got):
         g = cast_and_grad(r, b)
     t_ref, t_got = ref.trainer, got.trainer
