@@ -1,0 +1,107 @@
+"""The calls on two streams at once, as a runtime that decouples casting from
+the rest of the step would issue them (the paper's decoupled casting,
+Sec. IV-B, across steps): the next batch's Tensor Casting on a side stream,
+into a second set of cast outputs, while the current batch's forward and
+backward + update run on the main stream. The library keeps no state between
+calls besides the buffers the caller passes, so the table and accumulator
+after every step, and every step's pooled output, must equal the
+stream-ordered step's bit for bit (which the other tests check against the
+oracle)."""
+import pytest
+import torch
+
+from paper_2010_13100_amd import device_fill, tc
+from paper_2010_13100_amd import workload as wl
+from tests.gpu_harness import to_dev
+
+pytestmark = pytest.mark.gpu
+
+W = wl.WORKLOADS
+
+
+def cast_set(like, dev):
+    i32 = dict(dtype=torch.int32, device=dev)
+    return dict(unique_rows=torch.empty_like(like.unique_rows),
+                seg_offsets=torch.empty_like(like.seg_offsets),
+                casted_src=torch.empty_like(like.casted_src), num_unique=torch.zeros(1, **i32))
+
+
+@pytest.mark.parametrize("optimizer", ["sgd", "adagrad"])
+def test_side_stream_cast_matches_stream_order(optimizer):
+    w = W["c2"].scaled(name=f"streams-{optimizer}", num_tables=2, rows_per_table=20_000,
+                       batch=512, optimizer=optimizer)
+    steps = 4
+    batches = [wl.make_batch(w, s) for s in range(steps)]
+    print(f"\n[streams] {w.name}: pairs {[b.num_pairs for b in batches]}", flush=True)
+    dev = torch.device("cuda", 0)
+    max_pairs = max(b.num_pairs for b in batches)
+
+    def trainer():
+        t = tc.EmbeddingTrainer(total_rows=w.total_rows, dim=w.dim, num_tables=w.num_tables,
+                                bags_per_table=w.batch, max_pairs=max_pairs,
+                                optimizer=w.optimizer, lr=w.lr, eps=w.eps, gamma=w.gamma,
+                                device=dev, max_table_rows=w.rows_per_table)
+        device_fill.fill_uniform(t.W, seed=0, lo=w.init_lo, hi=w.init_hi)
+        return t
+
+    dbat = [dict(off=to_dev(b.table_row_offset), idx=to_dev(b.indices),
+                 bo=to_dev(b.bag_offsets), grad=to_dev(b.grad_out), n=b.num_pairs)
+            for b in batches]
+    main = torch.cuda.current_stream()
+
+    # stream-ordered: forward + cast, then backward + update, step after step
+    ref = trainer()
+    ref_out, ref_W, ref_A = [], [], []
+    for d in dbat:
+        ref.forward_cast(d["off"], d["idx"], d["bo"], d["n"], main)
+        ref.backward_update(d["grad"], main)
+        ref_out.append(ref.out.clone())
+        ref_W.append(ref.W.clone())
+        ref_A.append(ref.A.clone() if ref.A is not None else None)
+    torch.cuda.synchronize()
+
+    # two streams: cast(i + 1) on the side stream beside forward(i) and
+    # backward + update(i), each step's outputs in set i % 2
+    t = trainer()
+    side = torch.cuda.Stream()
+    sets = [dict(unique_rows=t.unique_rows, seg_offsets=t.seg_offsets,
+                 casted_src=t.casted_src, num_unique=t.num_unique), cast_set(t, dev)]
+    side_ws = torch.empty_like(t.workspace)
+
+    def cast(d, s, ws, stream):
+        tc.tc_cast_index(d["off"], t.num_tables, t.bags_per_table, t.total_rows,
+                         t.max_table_rows, d["idx"], d["bo"], d["n"], s["unique_rows"],
+                         s["seg_offsets"], s["casted_src"], None, s["num_unique"], ws, stream)
+
+    e_cast = [torch.cuda.Event() for _ in range(steps)]
+    e_bwd = [torch.cuda.Event() for _ in range(steps)]
+    cast(dbat[0], sets[0], t.workspace, main)
+    e_cast[0].record(main)
+    got_out, got_W, got_A = [], [], []
+    for i, d in enumerate(dbat):
+        if i + 1 < steps:
+            with torch.cuda.stream(side):
+                # set (i + 1) % 2 was last read by the backward of step i - 1
+                side.wait_event(e_bwd[i - 1] if i >= 1 else e_cast[0])
+                cast(dbat[i + 1], sets[(i + 1) % 2], side_ws, side)
+                e_cast[i + 1].record(side)
+        main.wait_event(e_cast[i])
+        s = sets[i % 2]
+        tc.tc_embed_forward(t.W, d["off"], t.num_tables, t.bags_per_table, d["idx"], d["bo"],
+                            t.out, main)
+        tc.tc_embed_backward_update(d["grad"], s["seg_offsets"], s["casted_src"],
+                                    s["unique_rows"], s["num_unique"], t.max_unique, t.W, t.A,
+                                    t.opt_kind, t.lr, t.eps, t.gamma, None, t.bwd_workspace,
+                                    main)
+        e_bwd[i].record(main)
+        got_out.append(t.out.clone())
+        got_W.append(t.W.clone())
+        got_A.append(t.A.clone() if t.A is not None else None)
+    torch.cuda.synchronize()
+
+    for i in range(steps):
+        print(f"[streams] step {i}", flush=True)
+        assert torch.equal(got_out[i], ref_out[i]), f"step {i}: pooled output differs"
+        assert torch.equal(got_W[i], ref_W[i]), f"step {i}: table differs"
+        if ref_A[i] is not None:
+            assert torch.equal(got_A[i], ref_A[i]), f"step {i}: accumulator differs"
