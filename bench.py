@@ -533,7 +533,8 @@ def compact(res):
             "step_hbm": {k: v for k, v in res["step_hbm"].items() if k.endswith("frac")},
             "dominant_call": r["call"], "dominant_algorithmic_frac": r["frac"],
             "dominant_counter_frac": r["traffic_frac"],
-            "dominant_compulsory_frac": r["compulsory_frac"]}
+            "dominant_compulsory_frac": r["compulsory_frac"],
+            **({"pipelined": res["pipelined"]} if "pipelined" in res else {})}
 
 
 def run_sweep(args, base, cfg_name, dev):
@@ -571,6 +572,63 @@ def run_sweep(args, base, cfg_name, dev):
         torch.cuda.empty_cache()
 
 
+def measure_pipelined(args, trainer, dbat, stream, mode):
+    """Steps with the next batch's cast on a side stream (the paper's
+    decoupled casting, Sec. IV-B, across steps), into a second slot of cast
+    outputs; the forward runs as its own call. mode "step": cast(i + 1)
+    beside forward(i) and backward + update(i) (it waits only for the
+    backward of step i - 1, the last reader of its slot); mode "backward":
+    cast(i + 1) waits for forward(i) and runs beside backward + update(i).
+    Same table bits as the stream-ordered step. Returns steps/s and ms/step
+    over args.steps steps (after args.warmup)."""
+    import torch
+
+    side = torch.cuda.Stream()
+    trainer.cast_slots(2)
+
+    def run(i0, n):
+        e_cast = [torch.cuda.Event() for _ in range(n)]
+        e_mark = [torch.cuda.Event() for _ in range(n)]
+        d0 = dbat[i0 % NUM_BATCHES]
+        trainer.cast(d0["off"], d0["idx"], d0["bo"], d0["n"], stream, slot=i0 % 2)
+        e_cast[0].record(stream)
+        for k in range(n):
+            i = i0 + k
+            d = dbat[i % NUM_BATCHES]
+            if mode == "backward":
+                stream.wait_event(e_cast[k])
+                trainer.forward(d["off"], d["idx"], d["bo"], stream)
+                e_mark[k].record(stream)
+            if k + 1 < n:
+                dn = dbat[(i + 1) % NUM_BATCHES]
+                with torch.cuda.stream(side):
+                    if mode == "backward":
+                        side.wait_event(e_mark[k])
+                    else:
+                        side.wait_event(e_mark[k - 1] if k >= 1 else e_cast[0])
+                    trainer.cast(dn["off"], dn["idx"], dn["bo"], dn["n"], side,
+                                 slot=(i + 1) % 2)
+                    e_cast[k + 1].record(side)
+            if mode == "step":
+                stream.wait_event(e_cast[k])
+                trainer.forward(d["off"], d["idx"], d["bo"], stream)
+            trainer.backward_update(d["grad"], stream, slot=i % 2)
+            if mode == "step":
+                e_mark[k].record(stream)
+
+    if args.warmup:
+        run(0, args.warmup)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    run(args.warmup, args.steps)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(stop) / args.steps
+    return {"schedule": mode, "steps_per_s": round(1000.0 / ms_step, 3),
+            "ms_per_step": round(ms_step, 5)}
+
+
 def run_workload(args, cfg_name, dev, keep_batch=False):
     """Set up one workload, time its step, free its device memory. Returns
     (result line, batch 0 if keep_batch else None)."""
@@ -586,6 +644,10 @@ def run_workload(args, cfg_name, dev, keep_batch=False):
     stream = torch.cuda.current_stream(dev)
     res = measure_step(args, w, cfg_name, trainer, dbat, stream, step_calls(args, w),
                        traffic_key)
+    if args.pipeline != "none" and w.optimizer != "rowwise_adagrad":
+        print(f"[bench] {cfg_name}: pipelined cast ({args.pipeline})", file=sys.stderr,
+              flush=True)
+        res["pipelined"] = measure_pipelined(args, trainer, dbat, stream, args.pipeline)
     keep = batches[0] if keep_batch else None
     del trainer, dbat, batches
     torch.cuda.synchronize()
@@ -653,6 +715,11 @@ def main():
                          "tc_embed_backward, tc_sparse_update")
     ap.add_argument("--no-overlap", action="store_true",
                     help="forward and cast as two calls (tc_embed_forward, tc_cast_index)")
+    ap.add_argument("--pipeline", default="backward", choices=["step", "backward", "none"],
+                    help="also time steps with the next batch's cast on a side stream, beside "
+                         "its backward + update ('backward', the default) or beside the whole "
+                         "step ('step'); reported under 'pipelined' beside the stream-ordered "
+                         "step, which stays the line's value ('none' skips it)")
     ap.add_argument("--optimizer", default=None,
                     choices=["sgd", "adagrad", "rmsprop", "rowwise_adagrad"],
                     help="replace the workload's optimizer (row-wise Adagrad runs unfused)")

@@ -282,17 +282,32 @@ class EmbeddingTrainer:
         bws = tc_backward_workspace_bytes(max_pairs, dim) if split_long else 0
         self.bwd_workspace = (torch.empty(bws, dtype=torch.uint8, device=device) if bws
                               else None)
+        # cast outputs by slot: slot 0 is the attributes above; cast_slots()
+        # adds more, so that the next batch can be cast (on another stream)
+        # while a step still reads the current one
+        self._slots = [dict(unique_rows=self.unique_rows, seg_offsets=self.seg_offsets,
+                            casted_src=self.casted_src, num_unique=self.num_unique)]
+
+    def cast_slots(self, n: int) -> None:
+        """Hold n sets of cast outputs (slots 0 .. n-1)."""
+        while len(self._slots) < n:
+            self._slots.append(dict(unique_rows=torch.empty_like(self.unique_rows),
+                                    seg_offsets=torch.empty_like(self.seg_offsets),
+                                    casted_src=torch.empty_like(self.casted_src),
+                                    num_unique=torch.zeros_like(self.num_unique)))
 
     def forward(self, table_row_offset, indices, bag_offsets, stream=None):
         tc_embed_forward(self.W, table_row_offset, self.num_tables, self.bags_per_table, indices,
                          bag_offsets, self.out, stream)
 
     def cast(self, table_row_offset, indices, bag_offsets, num_pairs, stream=None,
-             with_casted_dst=False):
+             with_casted_dst=False, slot=0):
+        c = self._slots[slot]
         tc_cast_index(table_row_offset, self.num_tables, self.bags_per_table, self.total_rows,
-                      self.max_table_rows, indices, bag_offsets, num_pairs, self.unique_rows,
-                      self.seg_offsets, self.casted_src, self.casted_dst if with_casted_dst else None,
-                      self.num_unique, self.workspace, stream)
+                      self.max_table_rows, indices, bag_offsets, num_pairs, c["unique_rows"],
+                      c["seg_offsets"], c["casted_src"],
+                      self.casted_dst if with_casted_dst else None, c["num_unique"],
+                      self.workspace, stream)
 
     def forward_cast(self, table_row_offset, indices, bag_offsets, num_pairs, stream=None,
                      with_casted_dst=False):
@@ -329,10 +344,12 @@ class EmbeddingTrainer:
                           self.num_unique, self.max_unique, self.coal, self.bwd_workspace,
                           stream)
 
-    def backward_update(self, grad_out, stream=None, store_coal=False):
-        """backward + update in one pass (coal stored only if store_coal)."""
-        tc_embed_backward_update(grad_out, self.seg_offsets, self.casted_src, self.unique_rows,
-                                 self.num_unique, self.max_unique, self.W, self.A, self.opt_kind,
+    def backward_update(self, grad_out, stream=None, store_coal=False, slot=0):
+        """backward + update in one pass (coal stored only if store_coal), on
+        the cast outputs in `slot`."""
+        c = self._slots[slot]
+        tc_embed_backward_update(grad_out, c["seg_offsets"], c["casted_src"], c["unique_rows"],
+                                 c["num_unique"], self.max_unique, self.W, self.A, self.opt_kind,
                                  self.lr, self.eps, self.gamma,
                                  self.coal if store_coal else None, self.bwd_workspace, stream)
 
