@@ -105,3 +105,69 @@ def test_side_stream_cast_matches_stream_order(optimizer):
         assert torch.equal(got_W[i], ref_W[i]), f"step {i}: table differs"
         if ref_A[i] is not None:
             assert torch.equal(got_A[i], ref_A[i]), f"step {i}: accumulator differs"
+
+
+@pytest.mark.parametrize("mode", ["backward", "step"])
+def test_trainer_slots_pipelined_matches_stream_order(mode):
+    """The schedules bench.py times as `pipelined`, through EmbeddingTrainer's
+    cast slots: the next batch cast on a side stream beside the backward +
+    update (mode "backward") or beside the whole step (mode "step")."""
+    w = W["c3"].scaled(name=f"slots-{mode}", num_tables=2, rows_per_table=30_000, batch=256)
+    steps = 5
+    batches = [wl.make_batch(w, s) for s in range(steps)]
+    print(f"\n[slots] {w.name}: pairs {[b.num_pairs for b in batches]}", flush=True)
+    dev = torch.device("cuda", 0)
+    max_pairs = max(b.num_pairs for b in batches)
+
+    def trainer():
+        t = tc.EmbeddingTrainer(total_rows=w.total_rows, dim=w.dim, num_tables=w.num_tables,
+                                bags_per_table=w.batch, max_pairs=max_pairs,
+                                optimizer=w.optimizer, lr=w.lr, eps=w.eps, gamma=w.gamma,
+                                device=dev, max_table_rows=w.rows_per_table)
+        device_fill.fill_uniform(t.W, seed=0, lo=w.init_lo, hi=w.init_hi)
+        return t
+
+    dbat = [dict(off=to_dev(b.table_row_offset), idx=to_dev(b.indices),
+                 bo=to_dev(b.bag_offsets), grad=to_dev(b.grad_out), n=b.num_pairs)
+            for b in batches]
+    main = torch.cuda.current_stream()
+    ref = trainer()
+    for d in dbat:
+        ref.forward_cast(d["off"], d["idx"], d["bo"], d["n"], main)
+        ref.backward_update(d["grad"], main)
+    ref_out = ref.out.clone()
+    torch.cuda.synchronize()
+
+    t = trainer()
+    t.cast_slots(2)
+    side = torch.cuda.Stream()
+    e_cast = [torch.cuda.Event() for _ in range(steps)]
+    e_mark = [torch.cuda.Event() for _ in range(steps)]
+    d0 = dbat[0]
+    t.cast(d0["off"], d0["idx"], d0["bo"], d0["n"], main, slot=0)
+    e_cast[0].record(main)
+    for i, d in enumerate(dbat):
+        if mode == "backward":
+            main.wait_event(e_cast[i])
+            t.forward(d["off"], d["idx"], d["bo"], main)
+            e_mark[i].record(main)
+        if i + 1 < steps:
+            dn = dbat[i + 1]
+            with torch.cuda.stream(side):
+                if mode == "backward":
+                    side.wait_event(e_mark[i])
+                else:
+                    side.wait_event(e_mark[i - 1] if i >= 1 else e_cast[0])
+                t.cast(dn["off"], dn["idx"], dn["bo"], dn["n"], side, slot=(i + 1) % 2)
+                e_cast[i + 1].record(side)
+        if mode == "step":
+            main.wait_event(e_cast[i])
+            t.forward(d["off"], d["idx"], d["bo"], main)
+        t.backward_update(d["grad"], main, slot=i % 2)
+        if mode == "step":
+            e_mark[i].record(main)
+    torch.cuda.synchronize()
+    assert torch.equal(t.out, ref_out), "last step's pooled output differs"
+    assert torch.equal(t.W, ref.W), "table differs"
+    if ref.A is not None:
+        assert torch.equal(t.A, ref.A), "accumulator differs"
